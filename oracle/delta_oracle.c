@@ -1,0 +1,405 @@
+/*
+ * delta_oracle.c -- plain fp64 CPU oracle of the Delta Attention prefill.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or
+ * call this file: only the tests, the smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header, table or helper with the
+ * GPU library.
+ *
+ * What it computes (Delta Attention: Fast and Accurate Sparse Attention
+ * Inference by Delta Correction, arXiv 2505.11254):
+ *
+ *   f  : dense causal softmax attention, scale 1/sqrt(d), keys j <= i
+ *        (Sec. 2, Eq. "attention"; causality: row i sees keys j <= i).
+ *   f* : StreamingLLM sparse attention -- sink tokens plus a sliding window,
+ *        softmax normalised over the selected keys only (Sec. 1-2 and the
+ *        normalisation remark before Lemma 1 in Sec. 3).
+ *        S(i) = { j <= i : j < n_sink  or  i - j < window }.
+ *   Algorithm 1 (Sec. 3):
+ *     1. A*V  <- f*(Q,K,V)                 for every row
+ *     2. Q~   <- every gamma-th row of Q   (Eq. "q-index-selection")
+ *     3. A~V  <- f(Q~,K,V)
+ *     4. Delta <- A~V - (A*V)_{i in delta}, delta = { i : i mod gamma = 0 }
+ *     5. out  <- A*V + repeat(Delta, gamma)   (Eq. "delta-final")
+ *   Implementation-details appendix: the last rows that do not fill a whole
+ *   group of gamma rows are computed densely, so the corrected part has a
+ *   length divisible by gamma.
+ *
+ * Readings taken where the paper is silent or garbled:
+ *   - positions are 0-based and local to each sequence; anchors are the rows
+ *     i with i mod gamma = 0, row i uses the anchor floor(i/gamma)*gamma <= i;
+ *   - the window holds `window` keys including the query itself (i - j < w);
+ *   - sinks are the first n_sink positions, united with the window;
+ *   - scale 1/sqrt(d) for both f and f* (Eq. 4 omits it; Eq. 1 has it);
+ *   - GQA: query head h reads kv head floor(h / (Hq/Hkv));
+ *   - tail rows [L_c, L), L_c = floor(L/gamma)*gamma, take the dense result.
+ *
+ * Arithmetic: every score, exponential, normaliser and output is fp64.
+ * Inputs are either fp64 or IEEE bfloat16 bit patterns, which are widened
+ * to fp64 exactly (a bfloat16 is the top half of a binary32).
+ * Softmax is two-pass per row: scores and their max, then exp(x - max),
+ * the normaliser Z and the weighted value sum.
+ *
+ * Layout: token-major contiguous tensors, q/out [T, Hq, d], k/v [T, Hkv, d];
+ * sequence b occupies rows [cu[b], cu[b+1]).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define DAO_OK 0
+#define DAO_ERR_ARG 1
+#define DAO_ERR_NOMEM 2
+
+#define DAO_MODE_DENSE 0
+#define DAO_MODE_SPARSE 1
+
+typedef struct {
+  const void* q;
+  const void* k;
+  const void* v;
+  int in_bf16; /* 1: inputs are bfloat16 bit patterns, 0: fp64 */
+  const int64_t* cu; /* host, B + 1 entries */
+  int B, Hq, Hkv, d;
+  int window, n_sink;
+} dao_problem;
+
+/* Widen element idx of an input tensor to fp64 (exact for bfloat16). */
+static inline double ld(const void* p, int bf16, int64_t idx) {
+  if (bf16) {
+    uint32_t u = ((uint32_t)((const uint16_t*)p)[idx]) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+  }
+  return ((const double*)p)[idx];
+}
+
+/* Key j (<= i) belongs to the key set of row i under the given mode. */
+static inline int key_in_set(int mode, int64_t i, int64_t j, int window, int n_sink) {
+  if (j > i) return 0;                 /* causal */
+  if (mode == DAO_MODE_DENSE) return 1;
+  return (j < n_sink) || (i - j < window);
+}
+
+/*
+ * One attention row: query row i (local) of head h in sequence b, over the
+ * key set of `mode`.  Writes o[d]; *m_out / *z_out receive the score max and
+ * the normaliser sum_j exp(x_j - m) when non-NULL; w_out (length i+1), when
+ * non-NULL, receives the softmax weight of every key j <= i (0 outside the
+ * set).  `x` is scratch of at least i+1 doubles.
+ */
+static void attn_row(const dao_problem* P, int mode, int b, int h, int64_t i,
+                     double* o, double* m_out, double* z_out, double* w_out, double* x) {
+  const int d = P->d;
+  const int G = P->Hq / P->Hkv;
+  const int g = h / G;
+  const int64_t base = P->cu[b];
+  const double tau = 1.0 / sqrt((double)d);
+  const int64_t qoff = ((base + i) * P->Hq + h) * (int64_t)d;
+
+  /* pass 1: scores over the key set and their max */
+  double m = -INFINITY;
+  for (int64_t j = 0; j <= i; ++j) {
+    if (!key_in_set(mode, i, j, P->window, P->n_sink)) continue;
+    const int64_t koff = ((base + j) * P->Hkv + g) * (int64_t)d;
+    double s = 0.0;
+#pragma omp simd reduction(+ : s)
+    for (int c = 0; c < d; ++c) s += ld(P->q, P->in_bf16, qoff + c) * ld(P->k, P->in_bf16, koff + c);
+    x[j] = tau * s;
+    if (x[j] > m) m = x[j];
+  }
+  /* pass 2: exponentials, normaliser, weighted values */
+  double z = 0.0;
+  for (int c = 0; c < d; ++c) o[c] = 0.0;
+  for (int64_t j = 0; j <= i; ++j) {
+    if (!key_in_set(mode, i, j, P->window, P->n_sink)) continue;
+    const double p = exp(x[j] - m);
+    z += p;
+    const int64_t voff = ((base + j) * P->Hkv + g) * (int64_t)d;
+#pragma omp simd
+    for (int c = 0; c < d; ++c) o[c] += p * ld(P->v, P->in_bf16, voff + c);
+  }
+  for (int c = 0; c < d; ++c) o[c] /= z;
+  if (m_out) *m_out = m;
+  if (z_out) *z_out = z;
+  if (w_out) {
+    for (int64_t j = 0; j <= i; ++j)
+      w_out[j] = key_in_set(mode, i, j, P->window, P->n_sink) ? exp(x[j] - m) / z : 0.0;
+  }
+}
+
+static int check_problem(const dao_problem* P) {
+  if (!P->q || !P->k || !P->v || !P->cu) return DAO_ERR_ARG;
+  if (P->B < 1 || P->Hq < 1 || P->Hkv < 1 || P->d < 1) return DAO_ERR_ARG;
+  if (P->Hq % P->Hkv != 0) return DAO_ERR_ARG;
+  if (P->window < 1 || P->n_sink < 0) return DAO_ERR_ARG;
+  for (int b = 0; b < P->B; ++b)
+    if (P->cu[b + 1] < P->cu[b]) return DAO_ERR_ARG;
+  return DAO_OK;
+}
+
+static int64_t max_len(const dao_problem* P) {
+  int64_t L = 0;
+  for (int b = 0; b < P->B; ++b)
+    if (P->cu[b + 1] - P->cu[b] > L) L = P->cu[b + 1] - P->cu[b];
+  return L;
+}
+
+/*
+ * Plain attention (f or f*) for every row, or for a list of rows.
+ * rows == NULL: out is [T, Hq, d]; m_out / z_out (optional) are [T, Hq].
+ * rows != NULL: n_rows triples (b, h, i_local); out is [n_rows, d];
+ *               m_out / z_out (optional) are [n_rows].
+ */
+int dao_attention(const void* q, const void* k, const void* v, int in_bf16,
+                  const int64_t* cu, int B, int Hq, int Hkv, int d,
+                  int window, int n_sink, int mode,
+                  const int64_t* rows, int64_t n_rows,
+                  double* out, double* m_out, double* z_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  if (mode != DAO_MODE_DENSE && mode != DAO_MODE_SPARSE) return DAO_ERR_ARG;
+  if (mode == DAO_MODE_DENSE) { P.window = 1; P.n_sink = 0; } /* unused by f */
+  if (check_problem(&P) != DAO_OK || !out) return DAO_ERR_ARG;
+  const int64_t T = cu[B];
+  const int64_t Lmax = max_len(&P);
+  int64_t n_items = rows ? n_rows : T * Hq;
+  int err = DAO_OK;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    if (!x) {
+#pragma omp atomic write
+      err = DAO_ERR_NOMEM;
+    }
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t it = 0; it < n_items; ++it) {
+      if (!x) continue;
+      int b, h;
+      int64_t i;
+      double *o, *mo, *zo;
+      if (rows) {
+        b = (int)rows[3 * it];
+        h = (int)rows[3 * it + 1];
+        i = rows[3 * it + 2];
+        o = out + it * d;
+        mo = m_out ? m_out + it : NULL;
+        zo = z_out ? z_out + it : NULL;
+      } else {
+        const int64_t t = it / Hq;
+        h = (int)(it % Hq);
+        b = 0;
+        while (cu[b + 1] <= t) ++b;
+        i = t - cu[b];
+        o = out + it * d;
+        mo = m_out ? m_out + it : NULL;
+        zo = z_out ? z_out + it : NULL;
+      }
+      if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= cu[b + 1] - cu[b]) {
+#pragma omp atomic write
+        err = DAO_ERR_ARG;
+        continue;
+      }
+      attn_row(&P, mode, b, h, i, o, mo, zo, NULL, x);
+    }
+    free(x);
+  }
+  return err;
+}
+
+/*
+ * Softmax weights of one row (b, h, i) under `mode`: w[j] for j = 0..i, zero
+ * outside the key set.  Used by the tests to check normalisation and support.
+ */
+int dao_attention_weights(const void* q, const void* k, const void* v, int in_bf16,
+                          const int64_t* cu, int B, int Hq, int Hkv, int d,
+                          int window, int n_sink, int mode, int b, int h, int64_t i,
+                          double* w, double* o) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  if (mode != DAO_MODE_DENSE && mode != DAO_MODE_SPARSE) return DAO_ERR_ARG;
+  if (mode == DAO_MODE_DENSE) { P.window = 1; P.n_sink = 0; } /* unused by f */
+  if (check_problem(&P) != DAO_OK || !w || !o) return DAO_ERR_ARG;
+  if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= cu[b + 1] - cu[b]) return DAO_ERR_ARG;
+  double* x = (double*)malloc(sizeof(double) * (size_t)(i + 1));
+  if (!x) return DAO_ERR_NOMEM;
+  attn_row(&P, mode, b, h, i, o, NULL, NULL, w, x);
+  free(x);
+  return DAO_OK;
+}
+
+/*
+ * Delta Attention, Algorithm 1, over whole sequences.
+ *   out    [T, Hq, d]  the corrected output (required)
+ *   sparse [T, Hq, d]  A*V for every row            (optional)
+ *   delta  [T, Hq, d]  the correction added to each row (optional; zero on
+ *                      tail rows, where the dense result replaces the row)
+ */
+int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16,
+                        const int64_t* cu, int B, int Hq, int Hkv, int d,
+                        int window, int n_sink, int gamma,
+                        double* out, double* sparse_out, double* delta_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  if (check_problem(&P) != DAO_OK || !out || gamma < 1) return DAO_ERR_ARG;
+  const int64_t T = cu[B];
+  const int64_t Lmax = max_len(&P);
+  double* sp = sparse_out ? sparse_out : (double*)malloc(sizeof(double) * (size_t)(T * Hq * d + 1));
+  if (!sp) return DAO_ERR_NOMEM;
+  int err = DAO_OK;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+  /* Step 1: A*V <- f*(Q, K, V) for every row of every sequence and head. */
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t it = 0; it < T * Hq; ++it) {
+      if (!x) {
+#pragma omp atomic write
+        err = DAO_ERR_NOMEM;
+        continue;
+      }
+      const int64_t t = it / Hq;
+      const int h = (int)(it % Hq);
+      int b = 0;
+      while (cu[b + 1] <= t) ++b;
+      attn_row(&P, DAO_MODE_SPARSE, b, h, t - cu[b], sp + it * d, NULL, NULL, NULL, x);
+    }
+    free(x);
+  }
+  if (err != DAO_OK) { if (!sparse_out) free(sp); return err; }
+
+  /* Steps 2-5, per sequence and head. */
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* dense = (double*)malloc(sizeof(double) * (size_t)d);
+    double* dl = (double*)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(dynamic, 1) collapse(2)
+    for (int b = 0; b < B; ++b) {
+      for (int h = 0; h < Hq; ++h) {
+        if (!x || !dense || !dl) {
+#pragma omp atomic write
+          err = DAO_ERR_NOMEM;
+          continue;
+        }
+        const int64_t L = cu[b + 1] - cu[b];
+        const int64_t Lc = (L / gamma) * gamma; /* corrected prefix */
+        /* Steps 2-4: for every anchor a in delta = {0, gamma, ...} < Lc, the
+         * dense row f(Q~_a) and Delta_a = A~V_a - (A*V)_a; step 5 adds Delta_a
+         * to the gamma rows a .. a+gamma-1 (repeat(Delta, gamma)). */
+        for (int64_t a = 0; a < Lc; a += gamma) {
+          attn_row(&P, DAO_MODE_DENSE, b, h, a, dense, NULL, NULL, NULL, x);
+          const double* spa = sp + ((cu[b] + a) * Hq + h) * (int64_t)d;
+          for (int c = 0; c < d; ++c) dl[c] = dense[c] - spa[c];
+          for (int64_t i = a; i < a + gamma; ++i) {
+            const int64_t off = ((cu[b] + i) * Hq + h) * (int64_t)d;
+            for (int c = 0; c < d; ++c) out[off + c] = sp[off + c] + dl[c];
+            if (delta_out)
+              for (int c = 0; c < d; ++c) delta_out[off + c] = dl[c];
+          }
+        }
+        /* Tail rows [Lc, L): computed densely (implementation-details appendix). */
+        for (int64_t i = Lc; i < L; ++i) {
+          const int64_t off = ((cu[b] + i) * Hq + h) * (int64_t)d;
+          attn_row(&P, DAO_MODE_DENSE, b, h, i, out + off, NULL, NULL, NULL, x);
+          if (delta_out)
+            for (int c = 0; c < d; ++c) delta_out[off + c] = 0.0;
+        }
+      }
+    }
+    free(x);
+    free(dense);
+    free(dl);
+  }
+  if (!sparse_out) free(sp);
+  return err;
+}
+
+/*
+ * Delta Attention at selected rows only: for each (b, h, i) the value row i
+ * of the full algorithm takes.  A row needs its own sparse key set and the
+ * dense and sparse results of its anchor floor(i/gamma)*gamma, so any subset
+ * is exact.  out is [n_rows, d]; delta (optional) is [n_rows, d].
+ */
+int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in_bf16,
+                             const int64_t* cu, int B, int Hq, int Hkv, int d,
+                             int window, int n_sink, int gamma,
+                             const int64_t* rows, int64_t n_rows,
+                             double* out, double* delta_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  if (check_problem(&P) != DAO_OK || !out || !rows || gamma < 1) return DAO_ERR_ARG;
+  const int64_t Lmax = max_len(&P);
+  int err = DAO_OK;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* sp_i = (double*)malloc(sizeof(double) * (size_t)d);
+    double* sp_a = (double*)malloc(sizeof(double) * (size_t)d);
+    double* dn_a = (double*)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t it = 0; it < n_rows; ++it) {
+      if (!x || !sp_i || !sp_a || !dn_a) {
+#pragma omp atomic write
+        err = DAO_ERR_NOMEM;
+        continue;
+      }
+      const int b = (int)rows[3 * it];
+      const int h = (int)rows[3 * it + 1];
+      const int64_t i = rows[3 * it + 2];
+      if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= cu[b + 1] - cu[b]) {
+#pragma omp atomic write
+        err = DAO_ERR_ARG;
+        continue;
+      }
+      const int64_t L = cu[b + 1] - cu[b];
+      const int64_t Lc = (L / gamma) * gamma;
+      double* o = out + it * d;
+      if (i >= Lc) { /* tail row: dense */
+        attn_row(&P, DAO_MODE_DENSE, b, h, i, o, NULL, NULL, NULL, x);
+        if (delta_out)
+          for (int c = 0; c < d; ++c) delta_out[it * d + c] = 0.0;
+        continue;
+      }
+      const int64_t a = (i / gamma) * gamma;
+      attn_row(&P, DAO_MODE_SPARSE, b, h, i, sp_i, NULL, NULL, NULL, x);   /* (A*V)_i */
+      attn_row(&P, DAO_MODE_SPARSE, b, h, a, sp_a, NULL, NULL, NULL, x);   /* (A*V)_a */
+      attn_row(&P, DAO_MODE_DENSE, b, h, a, dn_a, NULL, NULL, NULL, x);    /* (A~V)_a */
+      for (int c = 0; c < d; ++c) {
+        const double dl = dn_a[c] - sp_a[c];
+        o[c] = sp_i[c] + dl;
+        if (delta_out) delta_out[it * d + c] = dl;
+      }
+    }
+    free(x);
+    free(sp_i);
+    free(sp_a);
+    free(dn_a);
+  }
+  return err;
+}
+
+/* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
+int dao_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
