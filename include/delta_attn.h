@@ -1,0 +1,122 @@
+/*
+ * delta_attn.h -- C ABI of the MI355X (gfx950) Delta Attention prefill library.
+ *
+ * Delta Attention (arXiv 2505.11254, Sec. 3, Algorithm 1) corrects a sparse
+ * attention output with the difference between dense and sparse attention
+ * taken at every gamma-th query row:
+ *
+ *   out_i = (A*V)_i + [ (A~V)_a - (A*V)_a ],   a = floor(i/gamma)*gamma   (Eq. 6)
+ *
+ * where A*V is StreamingLLM attention (sink tokens + sliding window, softmax
+ * normalised over the selected keys) and A~V is dense causal attention
+ * evaluated only at the anchor rows a (Eq. 4).  Rows past the last whole
+ * group of gamma rows are computed densely (implementation-details appendix).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Tensors are token-major, contiguous, IEEE bfloat16 (bit patterns):
+ *   q, out : [T, Hq, d]      k, v : [T, Hkv, d]
+ * T = B*N for the fixed-length calls; T = cu_seqlens[B] for the _varlen
+ * calls, where sequence b occupies token rows [cu_seqlens[b], cu_seqlens[b+1]).
+ * All positions (causality, sinks, window, anchors) are local to a sequence;
+ * sequences never attend to each other.
+ *   - scale 1/sqrt(d) (Eq. 1), causal with the diagonal included (Sec. 2);
+ *   - GQA: query head h reads kv head floor(h / (Hq/Hkv));
+ *   - sparse key set of row i: { j <= i : j < n_sink  or  i - j < window };
+ *   - anchors: rows i with i mod gamma = 0 and i < floor(L/gamma)*gamma.
+ * d must be 64 or 128.  Every pointer is a device pointer, 16-byte aligned;
+ * the caller owns all memory.  `out` must not overlap q, k, v or the
+ * workspace.  `stream` is a hipStream_t (NULL: the null stream).
+ *
+ * Calls validate every argument before any HIP call; on error nothing is
+ * enqueued and `out` is untouched.  On success the work is only enqueued on
+ * `stream`; nothing synchronises.  Device faults surface at the caller's
+ * next synchronisation.  cu_seqlens (int32, B+1 entries, device) must start
+ * at 0 and be non-decreasing with every length <= max_seqlen; the library
+ * cannot check device-resident values, and violating this is undefined.
+ * Concurrent calls must not share a workspace.  No call keeps a pointer.
+ */
+#ifndef DELTA_ATTN_H
+#define DELTA_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DA_ABI_VERSION 1
+
+typedef enum {
+  DA_OK = 0,
+  DA_ERR_NULL = 1,        /* a required pointer is NULL */
+  DA_ERR_SHAPE = 2,       /* B, N/max_seqlen, Hq or Hkv < 1, Hq % Hkv != 0, or sizes overflow */
+  DA_ERR_PARAM = 3,       /* window < 1, n_sink < 0 or gamma < 1 */
+  DA_ERR_UNSUPPORTED = 4, /* d not in {64, 128}, or the current device is not gfx950 */
+  DA_ERR_ALIGN = 5,       /* a tensor or workspace pointer is not 16-byte aligned */
+  DA_ERR_WORKSPACE = 6,   /* workspace NULL or smaller than da_workspace_bytes() */
+  DA_ERR_HIP = 7          /* a HIP runtime call failed; see da_last_hip_error() */
+} da_status;
+
+/*
+ * Delta Attention prefill (Algorithm 1), fixed-length batch of B sequences
+ * of N tokens.  Writes the corrected output to `out`.
+ * workspace: device memory of at least da_workspace_bytes(B, N, Hq, Hkv, d,
+ * gamma) bytes, used for the strided rows' partial results and the sparse
+ * output at anchors; its contents on entry do not matter.
+ */
+da_status delta_attn_prefill(const void* q, const void* k, const void* v, void* out,
+                             int B, int Hq, int Hkv, int N, int d,
+                             int window, int n_sink, int gamma,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* As delta_attn_prefill for a ragged batch packed with cu_seqlens (device, int32). */
+da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v, void* out,
+                                    const int32_t* cu_seqlens, int B, int max_seqlen,
+                                    int Hq, int Hkv, int d, int window, int n_sink, int gamma,
+                                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Sparse attention alone (f*, StreamingLLM sink + window; the first step of
+ * Algorithm 1): out_i = (A*V)_i for every row.  Needs no workspace.
+ */
+da_status sparse_attn_prefill(const void* q, const void* k, const void* v, void* out,
+                              int B, int Hq, int Hkv, int N, int d, int window, int n_sink,
+                              void* stream);
+da_status sparse_attn_prefill_varlen(const void* q, const void* k, const void* v, void* out,
+                                     const int32_t* cu_seqlens, int B, int max_seqlen,
+                                     int Hq, int Hkv, int d, int window, int n_sink,
+                                     void* stream);
+
+/*
+ * Dense causal attention for every row (f, Eq. 1): the quadratic baseline the
+ * method is compared with (Sec. 4.1 latency study).  Needs no workspace.
+ */
+da_status dense_causal_attn_prefill(const void* q, const void* k, const void* v, void* out,
+                                    int B, int Hq, int Hkv, int N, int d, void* stream);
+da_status dense_causal_attn_prefill_varlen(const void* q, const void* k, const void* v,
+                                           void* out, const int32_t* cu_seqlens, int B,
+                                           int max_seqlen, int Hq, int Hkv, int d,
+                                           void* stream);
+
+/*
+ * Workspace bytes delta_attn_prefill[_varlen] needs for these sizes
+ * (max_seqlen = N for the fixed-length call).  0 if the sizes are invalid.
+ */
+size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma);
+
+/* Static, NUL-terminated name of a status code. */
+const char* da_status_string(da_status s);
+
+/* The hipError_t of the last DA_ERR_HIP on the calling thread (0 if none). */
+int da_last_hip_error(void);
+
+/* DA_ABI_VERSION of the loaded library. */
+int da_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DELTA_ATTN_H */

@@ -1,0 +1,162 @@
+"""ctypes binding of ``libdelta_attn.so`` (C ABI in ``include/delta_attn.h``).
+
+Argument marshalling only: every step of the attention path runs in the HIP
+kernels of the library.  torch supplies device memory and the stream.  There
+is no fallback: a missing library or a non-gfx950 device raises.
+
+Tensors are token-major bf16 on the GPU: q [T, Hq, d], k/v [T, Hkv, d].
+A fixed-length batch passes ``B`` (T = B * N); a ragged batch passes
+``cu_seqlens`` (int32, B + 1 entries, on the GPU) and ``max_seqlen``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdelta_attn.so")
+
+STATUS = {0: "DA_OK", 1: "DA_ERR_NULL", 2: "DA_ERR_SHAPE", 3: "DA_ERR_PARAM",
+          4: "DA_ERR_UNSUPPORTED", 5: "DA_ERR_ALIGN", 6: "DA_ERR_WORKSPACE", 7: "DA_ERR_HIP"}
+
+# C entry points and their argument types: p = pointer, i = int, z = size_t
+SIGNATURES = {
+    "delta_attn_prefill": "ppppiiiiiiiipzp",
+    "delta_attn_prefill_varlen": "pppppiiiiiiiipzp",
+    "sparse_attn_prefill": "ppppiiiiiiip",
+    "sparse_attn_prefill_varlen": "pppppiiiiiiip",
+    "dense_causal_attn_prefill": "ppppiiiiip",
+    "dense_causal_attn_prefill_varlen": "pppppiiiiip",
+}
+
+
+class DeltaAttnError(RuntimeError):
+    def __init__(self, fn, status, hip_error=0):
+        self.status = status
+        self.hip_error = hip_error
+        msg = f"{fn} returned {STATUS.get(status, status)}"
+        if status == 7:
+            msg += f" (hipError_t {hip_error})"
+        super().__init__(msg)
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "(hipcc for gfx950); there is no fallback implementation")
+    lib = ctypes.CDLL(path)
+    codes = {"p": ctypes.c_void_p, "i": ctypes.c_int, "z": ctypes.c_size_t}
+    for name, sig in SIGNATURES.items():
+        f = getattr(lib, name)
+        f.argtypes = [codes[c] for c in sig]
+        f.restype = ctypes.c_int
+    lib.da_workspace_bytes.argtypes = [ctypes.c_int] * 6
+    lib.da_workspace_bytes.restype = ctypes.c_size_t
+    lib.da_status_string.argtypes = [ctypes.c_int]
+    lib.da_status_string.restype = ctypes.c_char_p
+    lib.da_last_hip_error.argtypes = []
+    lib.da_last_hip_error.restype = ctypes.c_int
+    lib.da_abi_version.argtypes = []
+    lib.da_abi_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _call(name, *args):
+    lib = load_library()
+    rc = getattr(lib, name)(*args)
+    if rc != 0:
+        raise DeltaAttnError(name, rc, lib.da_last_hip_error())
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(device, stream):
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _shapes(q, k, v, B, cu_seqlens, max_seqlen):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dim() != 3:
+            raise ValueError(f"{name} must be [T, H, d]")
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    if cu_seqlens is None:
+        B = 1 if B is None else int(B)
+        if B < 1 or T % B != 0:
+            raise ValueError("T must be a multiple of B for a fixed-length batch")
+        return B, T // B, Hq, Hkv, d
+    if max_seqlen is None:
+        raise ValueError("max_seqlen is required with cu_seqlens")
+    if cu_seqlens.dtype != torch.int32:
+        raise ValueError("cu_seqlens must be int32")
+    return cu_seqlens.numel() - 1, int(max_seqlen), Hq, Hkv, d
+
+
+def workspace_bytes(B, max_seqlen, Hq, Hkv, d, gamma) -> int:
+    return int(load_library().da_workspace_bytes(B, max_seqlen, Hq, Hkv, d, gamma))
+
+
+def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=None,
+                       max_seqlen=None, out=None, workspace=None, stream=None):
+    """Delta Attention prefill (Algorithm 1); returns ``out`` [T, Hq, d] bf16."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    nbytes = workspace_bytes(B_, N, Hq, Hkv, d, gamma)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    wsz = workspace.numel() * workspace.element_size()
+    st = _stream(q.device, stream)
+    if cu_seqlens is None:
+        _call("delta_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), B_, Hq, Hkv, N, d,
+              window, n_sink, gamma, _ptr(workspace), wsz, st)
+    else:
+        _call("delta_attn_prefill_varlen", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+              _ptr(cu_seqlens), B_, N, Hq, Hkv, d, window, n_sink, gamma, _ptr(workspace),
+              wsz, st)
+    return out
+
+
+def sparse_attn_prefill(q, k, v, *, window, n_sink, B=None, cu_seqlens=None, max_seqlen=None,
+                        out=None, stream=None):
+    """Sink + sliding-window attention for every row (the f* of the paper)."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    st = _stream(q.device, stream)
+    if cu_seqlens is None:
+        _call("sparse_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), B_, Hq, Hkv, N, d,
+              window, n_sink, st)
+    else:
+        _call("sparse_attn_prefill_varlen", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+              _ptr(cu_seqlens), B_, N, Hq, Hkv, d, window, n_sink, st)
+    return out
+
+
+def dense_causal_attn_prefill(q, k, v, *, B=None, cu_seqlens=None, max_seqlen=None, out=None,
+                              stream=None):
+    """Dense causal attention for every row (the quadratic baseline f)."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    st = _stream(q.device, stream)
+    if cu_seqlens is None:
+        _call("dense_causal_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), B_, Hq, Hkv,
+              N, d, st)
+    else:
+        _call("dense_causal_attn_prefill_varlen", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+              _ptr(cu_seqlens), B_, N, Hq, Hkv, d, st)
+    return out

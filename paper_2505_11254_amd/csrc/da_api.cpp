@@ -1,0 +1,276 @@
+// da_api.cpp -- the C ABI of include/delta_attn.h: argument validation,
+// workspace planning and the launch sequence of the Delta Attention prefill.
+#include <math.h>
+#include <string.h>
+
+#include <atomic>
+
+#include "../../include/delta_attn.h"
+#include "da_internal.hpp"
+
+namespace da {
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+// Per-device answer to "is this a gfx950": 0 unknown, 1 yes, 2 no.
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_arch_ok[kMaxDevices];
+
+da_status fail_hip(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return DA_ERR_HIP;
+}
+
+da_status check_device() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail_hip(e);
+  if (dev < 0 || dev >= kMaxDevices) return DA_ERR_UNSUPPORTED;
+  int st = g_arch_ok[dev].load(std::memory_order_relaxed);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return fail_hip(e);
+    st = (strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+    g_arch_ok[dev].store(st, std::memory_order_relaxed);
+  }
+  return st == 1 ? DA_OK : DA_ERR_UNSUPPORTED;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+int heads_per_block(int G) {
+  if (G % 4 == 0) return 4;
+  if (G % 2 == 0) return 2;
+  return 1;
+}
+
+// Workspace of the Delta path.  Dense rows of a sequence of length L are the
+// floor(L/gamma) anchors plus the L mod gamma tail rows.  Their key axis is
+// split into nC chunks of `chunk` keys so that short sequences still give the
+// GPU enough workgroups; nC is chosen for about 16K (row tile x chunk) units
+// and capped so the partial results stay within 4 GiB.
+bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p) {
+  if (B < 1 || max_seqlen < 1 || Hq < 1 || Hkv < 1 || gamma < 1 || (d != 64 && d != 128))
+    return false;
+  if (Hq % Hkv != 0) return false;
+  const int64_t nA_max = max_seqlen / gamma;
+  const int64_t nR_max = nA_max + (int64_t)((gamma - 1 < max_seqlen) ? gamma - 1 : max_seqlen);
+  const int hpw = heads_per_block(Hq / Hkv);
+  const int64_t rows_per_block = (int64_t)kRowsPerWave * (kWavesPerBlock / hpw);
+  const int64_t rtiles = (nR_max + rows_per_block - 1) / rows_per_block;
+  const int64_t units = (int64_t)B * (Hq / hpw) * rtiles;
+  int64_t nC = (16384 + units - 1) / units;
+  if (nC > 16) nC = 16;
+  const int64_t max_chunks = (max_seqlen + kKeyTile * 32 - 1) / (kKeyTile * 32);  // >= 2048 keys each
+  if (nC > max_chunks) nC = max_chunks;
+  if (nC < 1) nC = 1;
+  const int64_t per_chunk_bytes = (int64_t)B * Hq * nR_max * (d + 2) * 4;
+  const int64_t budget = (int64_t)4 << 30;
+  while (nC > 1 && per_chunk_bytes * nC > budget) --nC;
+  int64_t chunk = (max_seqlen + nC - 1) / nC;
+  chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
+  nC = (max_seqlen + chunk - 1) / chunk;
+  p->nA_max = (int)nA_max;
+  p->nR_max = (int)nR_max;
+  p->nC = (int)nC;
+  p->chunk = (int)chunk;
+  p->sa_floats = (size_t)B * Hq * nA_max * d;
+  p->part_o_floats = (size_t)B * Hq * nR_max * nC * d;
+  p->part_ml_floats = (size_t)B * Hq * nR_max * nC * 2;
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  p->bytes = up(p->sa_floats * 4) + up(p->part_o_floats * 4) + up(p->part_ml_floats * 4);
+  return true;
+}
+
+namespace {
+
+struct Problem {
+  const void *q, *k, *v;
+  void* out;
+  const int32_t* cu;
+  int B, N, Hq, Hkv, d;
+  int window, n_sink, gamma;
+};
+
+// Shape/parameter checks shared by all calls; no HIP call happens here.
+da_status validate(const Problem& P, bool need_window, bool need_gamma) {
+  if (!P.q || !P.k || !P.v || !P.out) return DA_ERR_NULL;
+  if (P.B < 1 || P.N < 1 || P.Hq < 1 || P.Hkv < 1 || P.Hq % P.Hkv != 0) return DA_ERR_SHAPE;
+  if (need_window && (P.window < 1 || P.n_sink < 0)) return DA_ERR_PARAM;
+  if (need_gamma && P.gamma < 1) return DA_ERR_PARAM;
+  if (P.d != 64 && P.d != 128) return DA_ERR_UNSUPPORTED;
+  // token indices and row-tile counts are 32-bit inside the kernels
+  if (!P.cu && (int64_t)P.B * P.N > INT32_MAX) return DA_ERR_SHAPE;
+  const int hpw = heads_per_block(P.Hq / P.Hkv);
+  const int64_t rows_per_block = (int64_t)kRowsPerWave * (kWavesPerBlock / hpw);
+  const int64_t blocks = (int64_t)P.B * (P.Hq / hpw) * ((P.N + rows_per_block - 1) / rows_per_block);
+  if (blocks > INT32_MAX) return DA_ERR_SHAPE;
+  if (!aligned16(P.q) || !aligned16(P.k) || !aligned16(P.v) || !aligned16(P.out))
+    return DA_ERR_ALIGN;
+  return DA_OK;
+}
+
+Args base_args(const Problem& P) {
+  Args a;
+  memset(&a, 0, sizeof a);
+  a.q = (const uint16_t*)P.q;
+  a.k = (const uint16_t*)P.k;
+  a.v = (const uint16_t*)P.v;
+  a.out = (uint16_t*)P.out;
+  a.cu = P.cu;
+  a.B = P.B;
+  a.N = P.N;
+  a.Hq = P.Hq;
+  a.Hkv = P.Hkv;
+  a.d = P.d;
+  a.window = P.window;
+  a.n_sink = P.n_sink;
+  a.gamma = P.gamma > 0 ? P.gamma : 1;
+  a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)P.d));
+  a.hpw = heads_per_block(P.Hq / P.Hkv);
+  a.ppw = kWavesPerBlock / a.hpw;
+  a.n_hgroups = P.Hq / a.hpw;
+  const int rows_per_block = kRowsPerWave * a.ppw;
+  a.n_rtiles = (P.N + rows_per_block - 1) / rows_per_block;
+  a.head_chunk = 8192 / P.d;
+  return a;
+}
+
+da_status run_plain(const Problem& P, bool sparse, void* stream) {
+  da_status st = validate(P, sparse, false);
+  if (st != DA_OK) return st;
+  st = check_device();
+  if (st != DA_OK) return st;
+  Args a = base_args(P);
+  hipError_t e = sparse ? launch_sparse(a, (hipStream_t)stream) : launch_dense(a, (hipStream_t)stream);
+  if (e != hipSuccess) return fail_hip(e);
+  return DA_OK;
+}
+
+da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, void* stream) {
+  da_status st = validate(P, true, true);
+  if (st != DA_OK) return st;
+  Plan plan;
+  if (!make_plan(P.B, P.N, P.Hq, P.Hkv, P.d, P.gamma, &plan)) return DA_ERR_SHAPE;
+  if (!workspace || workspace_bytes < plan.bytes) return DA_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return DA_ERR_ALIGN;
+  {
+    const int hpw = heads_per_block(P.Hq / P.Hkv);
+    const int64_t rows_per_block = (int64_t)kRowsPerWave * (kWavesPerBlock / hpw);
+    const int64_t rtiles = (plan.nR_max + rows_per_block - 1) / rows_per_block;
+    if ((int64_t)P.B * (P.Hq / hpw) * plan.nC * rtiles > INT32_MAX) return DA_ERR_SHAPE;
+    if ((int64_t)P.B * plan.nR_max * ((P.Hq + 8192 / P.d - 1) / (8192 / P.d)) > INT32_MAX)
+      return DA_ERR_SHAPE;
+  }
+  st = check_device();
+  if (st != DA_OK) return st;
+
+  Args a = base_args(P);
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  char* ws = (char*)workspace;
+  a.sa = (float*)ws;
+  a.part_o = (float*)(ws + up(plan.sa_floats * 4));
+  a.part_ml = (float*)(ws + up(plan.sa_floats * 4) + up(plan.part_o_floats * 4));
+  a.nA_max = plan.nA_max;
+  a.nR_max = plan.nR_max;
+  a.nC = plan.nC;
+  a.chunk = plan.chunk;
+  hipStream_t s = (hipStream_t)stream;
+
+  // Step 1: sparse attention for every row (+ fp32 copy at anchors).
+  hipError_t e = launch_sparse(a, s);
+  if (e != hipSuccess) return fail_hip(e);
+  // Step 2: dense attention at anchors and tail rows, key axis split in chunks.
+  Args ar = a;
+  ar.n_rtiles = (plan.nR_max + kRowsPerWave * a.ppw - 1) / (kRowsPerWave * a.ppw);
+  e = launch_dense_rows(ar, s);
+  if (e != hipSuccess) return fail_hip(e);
+  // Step 3: merge, Delta, broadcast-add in place.
+  e = launch_delta_epilogue(a, s);
+  if (e != hipSuccess) return fail_hip(e);
+  return DA_OK;
+}
+
+}  // namespace
+}  // namespace da
+
+using da::Problem;
+
+extern "C" {
+
+da_status delta_attn_prefill(const void* q, const void* k, const void* v, void* out, int B,
+                             int Hq, int Hkv, int N, int d, int window, int n_sink, int gamma,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  Problem P{q, k, v, out, nullptr, B, N, Hq, Hkv, d, window, n_sink, gamma};
+  return da::run_delta(P, workspace, workspace_bytes, stream);
+}
+
+da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v, void* out,
+                                    const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                    int Hkv, int d, int window, int n_sink, int gamma,
+                                    void* workspace, size_t workspace_bytes, void* stream) {
+  if (!cu_seqlens) return DA_ERR_NULL;
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
+  return da::run_delta(P, workspace, workspace_bytes, stream);
+}
+
+da_status sparse_attn_prefill(const void* q, const void* k, const void* v, void* out, int B,
+                              int Hq, int Hkv, int N, int d, int window, int n_sink,
+                              void* stream) {
+  Problem P{q, k, v, out, nullptr, B, N, Hq, Hkv, d, window, n_sink, 1};
+  return da::run_plain(P, true, stream);
+}
+
+da_status sparse_attn_prefill_varlen(const void* q, const void* k, const void* v, void* out,
+                                     const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                     int Hkv, int d, int window, int n_sink, void* stream) {
+  if (!cu_seqlens) return DA_ERR_NULL;
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, 1};
+  return da::run_plain(P, true, stream);
+}
+
+da_status dense_causal_attn_prefill(const void* q, const void* k, const void* v, void* out,
+                                    int B, int Hq, int Hkv, int N, int d, void* stream) {
+  Problem P{q, k, v, out, nullptr, B, N, Hq, Hkv, d, 1, 0, 1};
+  return da::run_plain(P, false, stream);
+}
+
+da_status dense_causal_attn_prefill_varlen(const void* q, const void* k, const void* v,
+                                           void* out, const int32_t* cu_seqlens, int B,
+                                           int max_seqlen, int Hq, int Hkv, int d,
+                                           void* stream) {
+  if (!cu_seqlens) return DA_ERR_NULL;
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, 1, 0, 1};
+  return da::run_plain(P, false, stream);
+}
+
+size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma) {
+  da::Plan p;
+  if (!da::make_plan(B, max_seqlen, Hq, Hkv, d, gamma, &p)) return 0;
+  return p.bytes;
+}
+
+const char* da_status_string(da_status s) {
+  switch (s) {
+    case DA_OK: return "DA_OK";
+    case DA_ERR_NULL: return "DA_ERR_NULL";
+    case DA_ERR_SHAPE: return "DA_ERR_SHAPE";
+    case DA_ERR_PARAM: return "DA_ERR_PARAM";
+    case DA_ERR_UNSUPPORTED: return "DA_ERR_UNSUPPORTED";
+    case DA_ERR_ALIGN: return "DA_ERR_ALIGN";
+    case DA_ERR_WORKSPACE: return "DA_ERR_WORKSPACE";
+    case DA_ERR_HIP: return "DA_ERR_HIP";
+  }
+  return "DA_ERR_UNKNOWN";
+}
+
+int da_last_hip_error(void) { return da::g_last_hip_error; }
+
+int da_abi_version(void) { return DA_ABI_VERSION; }
+
+}  // extern "C"

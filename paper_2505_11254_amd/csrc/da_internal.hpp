@@ -1,0 +1,63 @@
+// da_internal.hpp -- launch arguments and plan shared by the C-ABI layer and
+// the gfx950 kernels.  Not part of the public interface.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace da {
+
+// Keys per tile of every attention kernel, and query rows per wavefront.
+constexpr int kKeyTile = 64;
+constexpr int kRowsPerWave = 32;
+constexpr int kWavesPerBlock = 4;
+constexpr int kThreads = 64 * kWavesPerBlock;
+
+// Everything a kernel needs; passed by value as the kernel argument.
+struct Args {
+  const uint16_t* q;  // [T, Hq, d] bf16
+  const uint16_t* k;  // [T, Hkv, d] bf16
+  const uint16_t* v;  // [T, Hkv, d] bf16
+  uint16_t* out;      // [T, Hq, d] bf16
+  const int32_t* cu;  // device cu_seqlens [B+1], or nullptr for B sequences of N tokens
+  int B, N;           // N: the fixed length, or max_seqlen when cu != nullptr
+  int Hq, Hkv, d;
+  int window, n_sink, gamma;
+  float scale_log2;   // log2(e) / sqrt(d): scores are exponentiated with exp2
+
+  // Workgroup tiling of (query heads x rows): hpw heads of one kv group, each
+  // with ppw sub-tiles of 32 rows; hpw * ppw == kWavesPerBlock.
+  int hpw, ppw;
+  int n_hgroups;      // Hq / hpw
+  int n_rtiles;       // row tiles (of 32 * ppw rows) per (sequence, head group)
+
+  // Workspace of the Delta path (nullptr for the plain attention calls).
+  float* sa;          // [B][Hq][nA_max][d]      sparse output at anchor rows, fp32
+  float* part_o;      // [B][Hq][nR_max][nC][d]  unnormalised partial outputs of dense rows
+  float* part_ml;     // [B][Hq][nR_max][nC][2]  (running max * scale_log2, normaliser)
+  int nA_max;         // max anchors per sequence: floor(max_seqlen / gamma)
+  int nR_max;         // max dense rows per sequence (anchors + tail rows)
+  int nC;             // key chunks per dense row (split of the key axis)
+  int chunk;          // keys per chunk, a multiple of kKeyTile
+  int head_chunk;     // query heads per epilogue workgroup
+};
+
+// Sizes of the Delta path's workspace for a problem; all in elements/bytes.
+struct Plan {
+  int nA_max, nR_max, nC, chunk;
+  size_t sa_floats, part_o_floats, part_ml_floats;
+  size_t bytes;
+};
+
+bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p);
+int heads_per_block(int G);
+
+// Kernel launchers (da_kernels.hip).  Each returns the hipError_t of the launch.
+hipError_t launch_sparse(const Args& a, hipStream_t s);
+hipError_t launch_dense(const Args& a, hipStream_t s);
+hipError_t launch_dense_rows(const Args& a, hipStream_t s);
+hipError_t launch_delta_epilogue(const Args& a, hipStream_t s);
+
+}  // namespace da

@@ -1,0 +1,491 @@
+// da_kernels.hip -- gfx950 (CDNA4) kernels of the Delta Attention prefill.
+//
+// Delta Attention (arXiv 2505.11254, Algorithm 1) runs three steps:
+//   1. sparse attention A*V for every query (StreamingLLM sinks + window),
+//   2. dense causal attention A~V for every gamma-th query row (Eq. 4),
+//   3. Delta = A~V - (A*V) at those rows, added to the gamma rows each covers
+//      (Eq. 6); rows after the last whole group are computed densely
+//      (implementation-details appendix).
+// Steps 1 and 2 and the dense causal baseline share one attention kernel
+// template (`attn_kernel`); step 3 is `delta_epilogue_kernel`.
+//
+// Tile core (one wavefront = 32 query rows, 64-key tiles, bf16 MFMA):
+//   S^T[key][row] = K Q^T   with v_mfma_f32_32x32x16_bf16: A = K rows from
+//                           LDS, B = the wave's Q rows held in registers;
+//   P^T = exp2(S^T * log2(e)/sqrt(d) - m)   online softmax in fp32;
+//   O^T[dim][row] += V^T P^T  A = V^T from LDS (stored transposed), B = P^T
+//                           taken straight from the S^T accumulator registers.
+// With this orientation a lane owns one query row in every accumulator
+// (lane % 32 = row), so the row max, the normaliser and the rescale of O
+// stay in the lane apart from one exchange with lane ^ 32, and P never goes
+// through LDS.  K/V tiles are double-buffered in LDS; each workgroup of four
+// waves shares every K/V tile between the query heads of one GQA group.
+#include "da_internal.hpp"
+
+#include <math.h>
+
+namespace da {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+enum Mode { kSparse = 0, kDense = 1, kDenseRows = 2 };
+
+// LDS layout of one pipeline stage (bf16 elements).  Rows are padded by 16
+// bytes so the 16-byte fragment reads of 32 consecutive rows hit distinct banks.
+template <int D>
+struct Lds {
+  static constexpr int kStride = D + 8;              // K tile row: one key, D dims
+  static constexpr int vStride = kKeyTile + 8;       // V^T tile row: one dim, 64 keys
+  static constexpr int kElems = kKeyTile * kStride;
+  static constexpr int vElems = D * vStride;
+  static constexpr int stageElems = kElems + vElems;
+  static constexpr int kLoads = kKeyTile * D / 8 / kThreads;  // 16-byte K loads per thread
+  static constexpr int vUnits = (kKeyTile / 4) * (D / 8);      // (4 keys x 8 dims) V units
+};
+
+struct Seq {
+  int64_t base;  // first token row of the sequence
+  int L;         // its length
+};
+
+__device__ __forceinline__ Seq seq_of(const Args& a, int b) {
+  if (a.cu) {
+    const int s0 = a.cu[b], s1 = a.cu[b + 1];
+    return {s0, s1 - s0};
+  }
+  return {(int64_t)b * a.N, a.N};
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8),
+// each with its own L2.  Give XCD x the contiguous logical range
+// [x*n/8, (x+1)*n/8) so neighbouring tiles, which read overlapping key/value
+// ranges, share one L2.
+__device__ __forceinline__ int64_t xcd_remap(int64_t i, int64_t n) {
+  const int64_t per = n / 8;
+  if (i < per * 8) return (i % 8) * per + i / 8;
+  return i;
+}
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Row index -> position of that row inside its sequence.  In the strided
+// dense-row mode row r < nA is anchor r*gamma, later rows are tail rows.
+template <int MODE>
+__device__ __forceinline__ int row_pos(int r, int nA, int Lc, int gamma) {
+  if (MODE == kDenseRows) return r < nA ? r * gamma : Lc + (r - nA);
+  return r;
+}
+
+template <int D, int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_kernel(Args a) {
+  using LD = Lds<D>;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * LD::stageElems];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int half = lane >> 5;
+  const int col = lane & 31;
+
+  // ---- which (sequence, head group, row tile[, key chunk]) this block owns
+  int64_t lid = xcd_remap(blockIdx.x, gridDim.x);
+  int rt = (int)(lid % a.n_rtiles);
+  lid /= a.n_rtiles;
+  int c = 0;
+  if (MODE == kDenseRows) {
+    c = (int)(lid % a.nC);
+    lid /= a.nC;
+  }
+  const int hg = (int)(lid % a.n_hgroups);
+  const int b = (int)(lid / a.n_hgroups);
+  if (MODE == kDense) rt = a.n_rtiles - 1 - rt;  // longest rows first
+
+  const Seq sq = seq_of(a, b);
+  const int L = sq.L;
+  const int G = a.Hq / a.Hkv;
+  const int h = hg * a.hpw + (wave % a.hpw);
+  const int g = (hg * a.hpw) / G;
+  const int sub = wave / a.hpw;
+  const int nA = L / a.gamma;
+  const int Lc = nA * a.gamma;
+  const int n_rows = (MODE == kDenseRows) ? nA + (L - Lc) : L;
+
+  const int rows_per_block = kRowsPerWave * a.ppw;
+  const int R0 = rt * rows_per_block;
+  if (R0 >= n_rows) return;  // uniform over the block
+  const int R1 = min(R0 + rows_per_block, n_rows);
+  const int bpos_lo = row_pos<MODE>(R0, nA, Lc, a.gamma);
+  const int bpos_hi = row_pos<MODE>(R1 - 1, nA, Lc, a.gamma);
+
+  // ---- key tiles the block visits: [ta0, ta1) then [tb0, tb1)
+  int ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
+  if (MODE == kSparse) {
+    const int sink_end = min(a.n_sink, bpos_hi + 1);
+    ta1 = (sink_end + kKeyTile - 1) / kKeyTile;
+    const int ws = max(0, bpos_lo - a.window + 1);
+    tb0 = max(ws / kKeyTile, ta1);
+    tb1 = max(tb0, bpos_hi / kKeyTile + 1);
+  } else if (MODE == kDense) {
+    ta1 = bpos_hi / kKeyTile + 1;
+  } else {
+    const int64_t kc0 = (int64_t)c * a.chunk;
+    if (kc0 > bpos_hi) return;  // this key chunk lies past every row of the block
+    const int64_t kc1 = min(kc0 + a.chunk, (int64_t)bpos_hi + 1);
+    ta0 = (int)(kc0 / kKeyTile);
+    ta1 = (int)((kc1 + kKeyTile - 1) / kKeyTile);
+  }
+  const int n_a = ta1 - ta0;
+  const int n_iter = n_a + (tb1 - tb0);
+
+  // ---- this wave's rows; lane (col) owns row wr0 + col
+  const int wr0 = R0 + sub * kRowsPerWave;
+  const bool wave_has_rows = wr0 < R1;
+  const int my_r = wr0 + col;
+  const bool row_valid = my_r < R1;
+  const int my_pos = row_valid ? row_pos<MODE>(my_r, nA, Lc, a.gamma) : -1;
+  const int wpos_lo = wave_has_rows ? row_pos<MODE>(wr0, nA, Lc, a.gamma) : 0;
+  const int wpos_hi = wave_has_rows ? row_pos<MODE>(min(wr0 + kRowsPerWave, R1) - 1, nA, Lc,
+                                                    a.gamma) : -1;
+
+  // Q fragments: lane holds dims kk*16 + half*8 .. +8 of its row, for every kk.
+  bf16x8 qf[D / 16];
+  {
+    const int64_t qrow = ((sq.base + (row_valid ? my_pos : 0)) * a.Hq + h) * (int64_t)D;
+    const uint16_t* qp = a.q + qrow + half * 8;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      u32x4 raw = row_valid ? *(const u32x4*)(qp + kk * 16) : u32x4{0u, 0u, 0u, 0u};
+      qf[kk] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
+
+  const int64_t kv_stride = (int64_t)a.Hkv * D;  // elements between consecutive keys
+  const uint16_t* kbase = a.k + (sq.base * a.Hkv + g) * (int64_t)D;
+  const uint16_t* vbase = a.v + (sq.base * a.Hkv + g) * (int64_t)D;
+
+  u32x4 kreg[LD::kLoads];
+  u32x4 vreg[4];
+
+  auto tile_at = [&](int it) { return it < n_a ? ta0 + it : tb0 + (it - n_a); };
+
+  // global -> registers: K as 16-byte row pieces, V as 4 keys x 8 dims per thread
+  auto gload = [&](int tile) {
+    const int key0 = tile * kKeyTile;
+#pragma unroll
+    for (int i = 0; i < LD::kLoads; ++i) {
+      const int u = tid + i * kThreads;
+      const int j = key0 + u / (D / 8);
+      const int ch = u % (D / 8);
+      kreg[i] = j < L ? *(const u32x4*)(kbase + j * kv_stride + ch * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+    if (tid < LD::vUnits) {
+      const int dc = tid % (D / 8);
+      const int kg = tid / (D / 8);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = key0 + kg * 4 + r;
+        vreg[r] = j < L ? *(const u32x4*)(vbase + j * kv_stride + dc * 8) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+
+  // registers -> LDS.  V is transposed to V^T[dim][key] so one 16-byte read
+  // gives a lane the 8 keys of its MFMA k-slots.  Inside each 16-key block the
+  // key groups 4..7 and 8..11 swap places: lane half h then finds keys
+  // {4h..4h+3, 8+4h..8+4h+3} contiguous, which is the order the S^T
+  // accumulator hands them over as P^T.
+  auto lds_store = [&](int buf) {
+    uint16_t* ks = smem + buf * LD::stageElems;
+    uint16_t* vs = ks + LD::kElems;
+#pragma unroll
+    for (int i = 0; i < LD::kLoads; ++i) {
+      const int u = tid + i * kThreads;
+      *(u32x4*)(ks + (u / (D / 8)) * LD::kStride + (u % (D / 8)) * 8) = kreg[i];
+    }
+    if (tid < LD::vUnits) {
+      const int dc = tid % (D / 8);
+      const int kg = tid / (D / 8);
+      const int sb = kg & 3;
+      const int pg = (kg & ~3) | ((sb == 1) ? 2 : (sb == 2) ? 1 : sb);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int w = e >> 1;
+        uint32_t lo, hi;
+        if (e & 1) {
+          lo = (vreg[0][w] >> 16) | (vreg[1][w] & 0xffff0000u);
+          hi = (vreg[2][w] >> 16) | (vreg[3][w] & 0xffff0000u);
+        } else {
+          lo = (vreg[0][w] & 0xffffu) | (vreg[1][w] << 16);
+          hi = (vreg[2][w] & 0xffffu) | (vreg[3][w] << 16);
+        }
+        *(u32x2*)(vs + (dc * 8 + e) * LD::vStride + pg * 4) = u32x2{lo, hi};
+      }
+    }
+  };
+
+  // 0: no key of the tile is visible to any row of the wave; 1: every key is
+  // visible to every row; 2: mixed, mask per element.
+  auto classify = [&](int tile) -> int {
+    if (!wave_has_rows) return 0;
+    const int k0 = tile * kKeyTile, k1 = k0 + kKeyTile - 1;
+    if (k0 > wpos_hi) return 0;
+    if (MODE == kSparse) {
+      if (k0 >= a.n_sink && wpos_lo - k1 >= a.window) return 0;
+      const bool full = k1 <= wpos_lo && (k1 < a.n_sink || wpos_hi - k0 < a.window);
+      return full ? 1 : 2;
+    }
+    return k1 <= wpos_lo ? 1 : 2;
+  };
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
+  float m = -INFINITY;  // running max of raw scores (same in lanes l and l^32)
+  float l = 0.f;        // this lane's share of the softmax normaliser
+  const float scale = a.scale_log2;
+
+  auto compute = [&](int buf, int tile, bool masked) {
+    const uint16_t* ks = smem + buf * LD::stageElems;
+    const uint16_t* vs = ks + LD::kElems;
+    f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const bf16x8 ka = *(const bf16x8*)(ks + col * LD::kStride + kk * 16 + half * 8);
+      const bf16x8 kb = *(const bf16x8*)(ks + (32 + col) * LD::kStride + kk * 16 + half * 8);
+      s0 = mfma32(ka, qf[kk], s0);
+      s1 = mfma32(kb, qf[kk], s1);
+    }
+    // accumulator register r of lane half h holds key 8*(r/4) + 4*h + r%4
+    if (masked) {
+      const int kbase_t = tile * kKeyTile + 4 * half;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j0 = kbase_t + 8 * (r >> 2) + (r & 3);
+        const int j1 = j0 + 32;
+        bool ok0 = j0 <= my_pos, ok1 = j1 <= my_pos;
+        if (MODE == kSparse) {
+          ok0 = ok0 && (j0 < a.n_sink || my_pos - j0 < a.window);
+          ok1 = ok1 && (j1 < a.n_sink || my_pos - j1 < a.window);
+        }
+        s0[r] = ok0 ? s0[r] : -INFINITY;
+        s1[r] = ok1 ? s1[r] : -INFINITY;
+      }
+    }
+    float mx = fmaxf(s0[0], s1[0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m, mx);
+    const bool none = (m_new == -INFINITY);
+    const float alpha = none ? 1.f : fast_exp2((m - m_new) * scale);
+    const float mc = none ? 0.f : m_new * scale;
+    m = m_new;
+    l *= alpha;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+    f32x16 p0, p1;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p0[r] = fast_exp2(fmaf(s0[r], scale, -mc));
+      p1[r] = fast_exp2(fmaf(s1[r], scale, -mc));
+      l += p0[r] + p1[r];
+    }
+    // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block t/2
+    bf16x8 pf[4];
+    pf[0] = __builtin_convertvector(p0.lo, bf16x8);
+    pf[1] = __builtin_convertvector(p0.hi, bf16x8);
+    pf[2] = __builtin_convertvector(p1.lo, bf16x8);
+    pf[3] = __builtin_convertvector(p1.hi, bf16x8);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb) {
+        const bf16x8 va = *(const bf16x8*)(vs + (32 * mb + col) * LD::vStride + 16 * t + 8 * half);
+        o[mb] = mfma32(va, pf[t], o[mb]);
+      }
+    }
+  };
+
+  // ---- double-buffered main loop: prefetch tile it+1 while computing tile it
+  if (n_iter > 0) {
+    gload(tile_at(0));
+    lds_store(0);
+  }
+  __syncthreads();
+  for (int it = 0; it < n_iter; ++it) {
+    const int buf = it & 1;
+    const int tile = tile_at(it);
+    if (it + 1 < n_iter) gload(tile_at(it + 1));
+    const int cls = classify(tile);
+    if (cls == 1)
+      compute(buf, tile, false);
+    else if (cls == 2)
+      compute(buf, tile, true);
+    if (it + 1 < n_iter) lds_store(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: output register r of block mb is dim 32*mb + 8*(r/4) + 4*half + r%4
+  const float lt = l + __shfl_xor(l, 32);
+  if (!row_valid) return;
+  if (MODE != kDenseRows) {
+    const float inv = 1.f / lt;
+    uint16_t* orow = a.out + ((sq.base + my_pos) * a.Hq + h) * (int64_t)D;
+    const bool write_sa = (MODE == kSparse) && a.sa && (my_pos % a.gamma == 0) && my_pos < Lc;
+    float* sarow = write_sa ? a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + my_pos / a.gamma) * D
+                            : nullptr;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb) {
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int dim = 32 * mb + 8 * jq + 4 * half;
+        f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
+                     o[mb][4 * jq + 3] * inv};
+        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+        *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
+        if (write_sa) *(f32x4*)(sarow + dim) = val;
+      }
+    }
+  } else {
+    const int64_t slot = (((int64_t)b * a.Hq + h) * a.nR_max + my_r) * a.nC + c;
+    float* po = a.part_o + slot * D;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb) {
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int dim = 32 * mb + 8 * jq + 4 * half;
+        *(f32x4*)(po + dim) = f32x4{o[mb][4 * jq], o[mb][4 * jq + 1], o[mb][4 * jq + 2],
+                                    o[mb][4 * jq + 3]};
+      }
+    }
+    if (half == 0) {
+      a.part_ml[slot * 2] = m * scale;  // -inf when no key of the chunk is visible
+      a.part_ml[slot * 2 + 1] = lt;
+    }
+  }
+}
+
+// Step 3 of Algorithm 1 for one dense row r of one sequence and a range of
+// heads: merge the key-chunk partials of r into the dense result (log-sum-exp
+// merge), then
+//   anchor row a = r*gamma:  Delta = dense - sparse(a) in fp32, out[a] = dense,
+//                            out[i] += Delta for i = a+1 .. a+gamma-1;
+//   tail row:                out[row] = dense.
+// An anchor with a < n_sink + window sees all keys 0..a in its sparse set, so
+// its Delta is exactly zero and the block leaves its rows untouched.
+template <int D>
+__global__ __launch_bounds__(kThreads) void delta_epilogue_kernel(Args a) {
+  __shared__ float delta[8192];  // [head in range][D]
+  const int tid = threadIdx.x;
+  int64_t lid = blockIdx.x;
+  const int n_hc = (a.Hq + a.head_chunk - 1) / a.head_chunk;
+  const int hc = (int)(lid % n_hc);
+  lid /= n_hc;
+  const int r = (int)(lid % a.nR_max);
+  const int b = (int)(lid / a.nR_max);
+
+  const Seq sq = seq_of(a, b);
+  const int L = sq.L;
+  const int nA = L / a.gamma;
+  const int Lc = nA * a.gamma;
+  const int nR = nA + (L - Lc);
+  if (r >= nR) return;
+  const bool anchor = r < nA;
+  const int pos = anchor ? r * a.gamma : Lc + (r - nA);
+  if (anchor && (int64_t)pos < (int64_t)a.n_sink + a.window) return;
+
+  const int h0 = hc * a.head_chunk;
+  const int h1 = min(a.Hq, h0 + a.head_chunk);
+  const int nh = h1 - h0;
+  const int nc = (int)(((int64_t)pos + a.chunk) / a.chunk);  // chunks holding keys 0..pos
+  constexpr int DC = D / 8;
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+
+  for (int idx = tid; idx < nh * DC; idx += kThreads) {
+    const int hh = idx / DC, dc = idx % DC;
+    const int h = h0 + hh;
+    const int64_t slot0 = (((int64_t)b * a.Hq + h) * a.nR_max + r) * a.nC;
+    float M = -INFINITY;
+    for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, a.part_ml[(slot0 + cc) * 2]);
+    float lsum = 0.f;
+    f32x8 acc = f32x8{};
+    for (int cc = 0; cc < nc; ++cc) {
+      const float mc = a.part_ml[(slot0 + cc) * 2];
+      if (mc == -INFINITY) continue;
+      const float w = fast_exp2(mc - M);
+      lsum += w * a.part_ml[(slot0 + cc) * 2 + 1];
+      const f32x8 po = *(const f32x8*)(a.part_o + (slot0 + cc) * D + dc * 8);
+      acc += w * po;
+    }
+    const f32x8 dense = acc * (1.f / lsum);
+    uint16_t* orow = a.out + ((sq.base + pos) * a.Hq + h) * (int64_t)D + dc * 8;
+    *(bf16x8_t*)orow = __builtin_convertvector(dense, bf16x8_t);
+    if (anchor) {
+      const f32x8 sp = *(const f32x8*)(a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + r) * D + dc * 8);
+      *(f32x8*)(delta + hh * D + dc * 8) = dense - sp;
+    }
+  }
+  if (!anchor) return;
+  __syncthreads();
+
+  // rows pos+1 .. pos+gamma-1 for heads [h0, h1): nh*D contiguous values per row
+  const int per_row = nh * DC;
+  const int64_t total = (int64_t)(a.gamma - 1) * per_row;
+  for (int64_t u = tid; u < total; u += kThreads) {
+    const int i = (int)(u / per_row);
+    const int rem = (int)(u % per_row);
+    const int hh = rem / DC, dc = rem % DC;
+    uint16_t* p = a.out + ((sq.base + pos + 1 + i) * a.Hq + h0 + hh) * (int64_t)D + dc * 8;
+    const bf16x8_t x = *(const bf16x8_t*)p;
+    const f32x8 y = __builtin_convertvector(x, f32x8) + *(const f32x8*)(delta + hh * D + dc * 8);
+    *(bf16x8_t*)p = __builtin_convertvector(y, bf16x8_t);
+  }
+}
+
+template <int MODE>
+hipError_t launch_attn(const Args& a, hipStream_t s, int64_t nblocks) {
+  if (nblocks <= 0) return hipSuccess;
+  if (a.d == 128)
+    hipLaunchKernelGGL((attn_kernel<128, MODE>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((attn_kernel<64, MODE>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sparse(const Args& a, hipStream_t s) {
+  return launch_attn<kSparse>(a, s, (int64_t)a.B * a.n_hgroups * a.n_rtiles);
+}
+
+hipError_t launch_dense(const Args& a, hipStream_t s) {
+  return launch_attn<kDense>(a, s, (int64_t)a.B * a.n_hgroups * a.n_rtiles);
+}
+
+hipError_t launch_dense_rows(const Args& a, hipStream_t s) {
+  return launch_attn<kDenseRows>(a, s, (int64_t)a.B * a.n_hgroups * a.nC * a.n_rtiles);
+}
+
+hipError_t launch_delta_epilogue(const Args& a, hipStream_t s) {
+  const int n_hc = (a.Hq + a.head_chunk - 1) / a.head_chunk;
+  const int64_t nblocks = (int64_t)a.B * a.nR_max * n_hc;
+  if (nblocks <= 0) return hipSuccess;
+  if (a.d == 128)
+    hipLaunchKernelGGL(delta_epilogue_kernel<128>, dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(delta_epilogue_kernel<64>, dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace da

@@ -1,0 +1,63 @@
+"""Row sampling and error metrics for parity checks against the oracle.
+
+A row of Delta Attention depends only on its own key set and on its
+anchor's sparse and dense rows, so the oracle can evaluate any subset of
+(sequence, head, row) triples exactly; large workloads are checked on such
+samples.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+# spec tolerances for bf16 I/O with fp32 accumulation
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+
+
+def sample_rows(seqlens, Hq, window, n_sink, gamma, n_random=96, seed=0):
+    """(b, h, i) triples: every boundary the method has, plus seeded random rows."""
+    rng = np.random.default_rng(seed)
+    rows = set()
+    for b, L in enumerate(seqlens):
+        Lc = (L // gamma) * gamma
+        first_open = -(-(n_sink + window) // gamma) * gamma  # first anchor with Delta != 0
+        special = [0, 1, gamma - 1, gamma, gamma + 1, first_open - gamma, first_open - 1,
+                   first_open, first_open + 1, first_open + gamma - 1, window - 1, window,
+                   window + 1, n_sink - 1, n_sink, n_sink + window - 1, n_sink + window,
+                   Lc - gamma, Lc - gamma + 1, Lc - 1, Lc, L - 2, L - 1]
+        for p in special + [int(x) for x in rng.integers(0, L, n_random)]:
+            if 0 <= p < L:
+                rows.add((b, int(rng.integers(0, Hq)), int(p)))
+        p = int(rng.integers(0, L))
+        rows |= {(b, h, p) for h in range(Hq)}
+    return sorted(rows)
+
+
+def gather_rows(out: torch.Tensor, cu, rows) -> np.ndarray:
+    """out[cu[b] + i, h] for every (b, h, i), as fp64 [n, d]."""
+    cu = [int(x) for x in cu]
+    t = torch.tensor([cu[b] + i for (b, h, i) in rows], dtype=torch.long, device=out.device)
+    hh = torch.tensor([h for (b, h, i) in rows], dtype=torch.long, device=out.device)
+    return out[t, hh].float().cpu().numpy().astype(np.float64)
+
+
+def errors(got: np.ndarray, ref: np.ndarray) -> dict:
+    e = np.abs(got - ref)
+    return {"max_abs": float(e.max()), "mean_abs": float(e.mean()),
+            "rel_l2": float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)),
+            "nan": int(np.isnan(got).sum())}
+
+
+def assert_parity(got, ref, what="", max_abs=MAX_ABS, mean_abs=MEAN_ABS):
+    if isinstance(got, torch.Tensor):
+        got = got.float().cpu().numpy().astype(np.float64)
+    err = errors(got, ref)
+    assert err["nan"] == 0, f"{what}: NaN in output {err}"
+    assert err["max_abs"] <= max_abs and err["mean_abs"] <= mean_abs, f"{what}: {err}"
+    return err
+
+
+def to_oracle_bits(t: torch.Tensor) -> np.ndarray:
+    """bf16 tensor (any device) -> uint16 numpy bit patterns the oracle widens exactly."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)

@@ -1,0 +1,131 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects bad arguments before touching the GPU.
+
+Every call here fails validation, which happens before any HIP call, so the
+fake device pointers below are never dereferenced and no kernel is launched.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "delta_attn.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2505_11254_amd import binding
+    return binding.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^[A-Za-z_][A-Za-z0-9_ \*]*?\b([a-z_][a-z0-9_]*)\s*\(", text, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "defined")))
+
+
+def test_header_declares_the_expected_entry_points():
+    names = declared_functions()
+    for n in ("delta_attn_prefill", "delta_attn_prefill_varlen", "sparse_attn_prefill",
+              "sparse_attn_prefill_varlen", "dense_causal_attn_prefill",
+              "dense_causal_attn_prefill_varlen", "da_workspace_bytes", "da_status_string",
+              "da_last_hip_error", "da_abi_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_binding_signatures_match_header_arity(lib):
+    from paper_2505_11254_amd import binding
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for name, sig in binding.SIGNATURES.items():
+        m = re.search(r"\b" + name + r"\s*\(([^;]*)\);", text, flags=re.S)
+        assert m, name
+        assert len(m.group(1).split(",")) == len(sig), name
+
+
+def test_abi_version_and_status_strings(lib):
+    assert lib.da_abi_version() == 1
+    assert lib.da_status_string(0) == b"DA_OK"
+    assert lib.da_status_string(6) == b"DA_ERR_WORKSPACE"
+    assert lib.da_last_hip_error() == 0
+
+
+FAKE = 0x100000  # 16-byte aligned, never dereferenced (validation fails first)
+
+
+def delta(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, out=FAKE, B=1, Hq=8, Hkv=2, N=1024, d=128, window=64,
+             n_sink=4, gamma=16, ws=FAKE, wsz=1 << 40)
+    a.update(kw)
+    return lib.delta_attn_prefill(a["q"], a["k"], a["v"], a["out"], a["B"], a["Hq"], a["Hkv"],
+                                  a["N"], a["d"], a["window"], a["n_sink"], a["gamma"],
+                                  a["ws"], a["wsz"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), 1), (dict(out=None), 1), (dict(v=None), 1),
+    (dict(B=0), 2), (dict(N=0), 2), (dict(Hq=0), 2), (dict(Hkv=0), 2), (dict(Hq=6, Hkv=4), 2),
+    (dict(B=70000, N=70000), 2),
+    (dict(window=0), 3), (dict(n_sink=-1), 3), (dict(gamma=0), 3),
+    (dict(d=96), 4), (dict(d=256), 4),
+    (dict(q=FAKE + 8), 5), (dict(out=FAKE + 2), 5), (dict(k=FAKE + 4), 5),
+    (dict(ws=None), 6), (dict(wsz=16), 6), (dict(ws=FAKE + 8), 5),
+])
+def test_delta_call_rejects_bad_arguments(lib, kw, status):
+    assert delta(lib, **kw) == status
+
+
+def test_varlen_requires_cu_seqlens(lib):
+    rc = lib.delta_attn_prefill_varlen(FAKE, FAKE, FAKE, FAKE, None, 2, 128, 8, 2, 128, 16, 2,
+                                       4, FAKE, 1 << 40, None)
+    assert rc == 1
+    assert lib.sparse_attn_prefill_varlen(FAKE, FAKE, FAKE, FAKE, None, 2, 128, 8, 2, 128, 16,
+                                          2, None) == 1
+    assert lib.dense_causal_attn_prefill_varlen(FAKE, FAKE, FAKE, FAKE, None, 2, 128, 8, 2,
+                                                128, None) == 1
+
+
+def test_plain_calls_reject_bad_arguments(lib):
+    assert lib.sparse_attn_prefill(FAKE, FAKE, FAKE, FAKE, 1, 8, 2, 128, 128, 0, 0, None) == 3
+    assert lib.sparse_attn_prefill(FAKE, FAKE, FAKE, FAKE, 1, 8, 3, 128, 128, 4, 0, None) == 2
+    assert lib.dense_causal_attn_prefill(FAKE, FAKE, FAKE, FAKE, 1, 8, 2, 128, 80, None) == 4
+    assert lib.dense_causal_attn_prefill(FAKE + 1, FAKE, FAKE, FAKE, 1, 8, 2, 128, 128,
+                                         None) == 5
+
+
+def test_workspace_size_properties(lib):
+    ws = lib.da_workspace_bytes
+    assert ws(0, 128, 8, 2, 128, 16) == 0
+    assert ws(1, 128, 8, 3, 128, 16) == 0
+    assert ws(1, 128, 8, 2, 96, 16) == 0
+    # at least the fp32 sparse rows at anchors plus one partial (d + 2 floats) per dense row
+    for (B, L, Hq, Hkv, d, g) in [(1, 1024, 1, 1, 64, 16), (1, 32768, 32, 8, 128, 64),
+                                   (4, 131072, 64, 8, 128, 32), (1, 1 << 20, 32, 8, 128, 64)]:
+        nA = L // g
+        assert ws(B, L, Hq, Hkv, d, g) >= B * Hq * (nA * d + (nA + g - 1) * (d + 2)) * 4
+        assert ws(B, L, Hq, Hkv, d, g) % 256 == 0
+    assert ws(1, 1 << 20, 32, 8, 128, 64) < (2 << 30)
+    assert ws(1, 4096, 8, 2, 128, 64) <= ws(1, 8192, 8, 2, 128, 64)
+
+
+def test_oracle_and_library_share_nothing():
+    """The oracle never imports the GPU package, and the GPU sources never name the oracle."""
+    osrc = open(os.path.join(ROOT, "oracle", "delta_oracle.c")).read()
+    opy = open(os.path.join(ROOT, "oracle", "__init__.py")).read()
+    assert "paper_2505_11254_amd" not in osrc + opy and "delta_attn.h" not in osrc
+    pkg = os.path.join(ROOT, "paper_2505_11254_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".hpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "delta_oracle" not in text, f
