@@ -1,0 +1,302 @@
+#!/usr/bin/env python3
+"""Benchmark of the Delta Attention prefill hot path on one MI355X.
+
+One step = one whole Delta Attention prefill (Algorithm 1: sparse attention
+for every row, dense attention at every gamma-th row, Delta correction) over
+one batch of synthetic inputs already resident in HBM.  The default workload
+is the 1M-token Llama-3.1-8B-shaped attention layer (Hq=32, Hkv=8, d=128,
+window 2048, 64 sinks, gamma 64), the length of the paper's latency study.
+
+Prints ONE JSON line on stdout:
+  value        prefill tokens/s per layer (whole job; one GPU)
+  roofline     the dominant kernel against the bf16 MFMA peak, from HIP
+               events on the stream the kernels run on
+  cpu_baseline the fp64 oracle timed on the host cores on a bounded sample,
+               extrapolated by exact key counts
+Everything else goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pair_counts(seqlens, window, n_sink, gamma):
+    """Per head: (sum_i |S(i)|, sum over dense rows of their key count, dense causal pairs)."""
+    import numpy as np
+    sp = dr = dc = 0
+    for L in seqlens:
+        i = np.arange(L, dtype=np.int64)
+        sinks = np.minimum(n_sink, i + 1)
+        win = np.minimum(window, np.maximum(i + 1 - sinks, 0))
+        sp += int((sinks + win).sum())
+        Lc = (L // gamma) * gamma
+        a = np.arange(0, Lc, gamma, dtype=np.int64)
+        t = np.arange(Lc, L, dtype=np.int64)
+        dr += int((a + 1).sum() + (t + 1).sum())
+        dc += L * (L + 1) // 2
+    return sp, dr, dc
+
+
+def epilogue_bytes(wl):
+    """Algorithmic HBM bytes of the Delta correction: for every group whose
+    anchor is not covered by the sparse key set, read and write the gamma-1
+    corrected bf16 rows, write the bf16 anchor row, read its fp32 sparse and
+    dense rows; dense tail rows are written once."""
+    tot = 0
+    for L in wl.seqlens:
+        nA = L // wl.gamma
+        first_open = -(-(wl.n_sink + wl.window) // wl.gamma)  # first anchor index with Delta
+        n_open = max(0, nA - first_open)
+        per_group = (wl.gamma - 1) * wl.d * 2 * 2 + wl.d * 2 + 2 * wl.d * 4
+        tot += n_open * per_group * wl.Hq + (L - nA * wl.gamma) * wl.d * 2 * wl.Hq
+    return tot
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("da_kernels.hip", "da_api.cpp", "da_internal.hpp"):
+        with open(os.path.join(ROOT, "paper_2505_11254_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM traffic per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    ent = rec.get(workload, {}).get(kernel)
+    if not ent or ent.get("source_hash") != kernel_source_hash():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, q, k, v, target_s=12.0):
+    """Time the fp64 oracle on sampled sparse rows and sampled anchor rows of the
+    workload, and extrapolate the whole-workload oracle time by exact key counts
+    (the full algorithm evaluates f* on every row and f on every anchor row)."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    bits = [x.contiguous().view(torch.int16).cpu().numpy().view(np.uint16) for x in (q, k, v)]
+    cu = np.asarray(wl.cu_seqlens(), dtype=np.int64)
+    rng = np.random.default_rng(1234)
+    nthreads = oracle.max_threads()
+    sp_pairs, dr_pairs, _ = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
+
+    def sample(n_sp, n_dn):
+        sp_rows, dn_rows, k_sp, k_dn = [], [], 0, 0
+        for _ in range(n_sp):
+            b = int(rng.integers(0, wl.B))
+            L = wl.seqlens[b]
+            i = int(rng.integers(min(L - 1, wl.n_sink + wl.window), L))
+            sp_rows.append((b, int(rng.integers(0, wl.Hq)), i))
+            k_sp += min(i + 1, wl.n_sink + wl.window)
+        for _ in range(n_dn):
+            b = int(rng.integers(0, wl.B))
+            L = wl.seqlens[b]
+            a = int(rng.integers(0, max(1, L // wl.gamma))) * wl.gamma
+            dn_rows.append((b, int(rng.integers(0, wl.Hq)), a))
+            k_dn += a + 1
+        t0 = time.perf_counter()
+        oracle.attention(*bits, cu, mode=oracle.MODE_SPARSE, window=wl.window,
+                         n_sink=wl.n_sink, rows=sp_rows)
+        t1 = time.perf_counter()
+        oracle.attention(*bits, cu, mode=oracle.MODE_DENSE, rows=dn_rows)
+        t2 = time.perf_counter()
+        return (t1 - t0) / max(k_sp, 1), (t2 - t1) / max(k_dn, 1), t2 - t0, k_sp, k_dn
+
+    # calibrate on a small sample, then size the timed sample to about target_s
+    c_sp, c_dn, _, _, _ = sample(4 * nthreads, nthreads)
+    est_sp = 0.5 * target_s / max(c_sp * (wl.n_sink + wl.window), 1e-12)
+    est_dn = 0.5 * target_s / max(c_dn * (max(wl.seqlens) / 2), 1e-12)
+    n_sp = int(min(max(est_sp, nthreads), 200000))
+    n_dn = int(min(max(est_dn, nthreads), 20000))
+    c_sp, c_dn, spent, k_sp, k_dn = sample(n_sp, n_dn)
+    if spent < 0.5 * target_s:  # the calibration sample was too small to size this one
+        f = min(target_s / max(spent, 1e-3), 20.0)
+        n_sp, n_dn = int(min(n_sp * f, 400000)), int(min(n_dn * f, 40000))
+        c_sp, c_dn, spent, k_sp, k_dn = sample(n_sp, n_dn)
+    t_full = (c_sp * sp_pairs + c_dn * dr_pairs) * wl.Hq
+    tokens = wl.total_tokens
+    return {
+        "value": tokens / t_full, "unit": "tokens/s", "cores": nthreads, "kind": "oracle",
+        "sample": (f"{n_sp} sparse rows ({k_sp} keys) and {n_dn} anchor dense rows "
+                   f"({k_dn} keys), random heads/positions of this workload, timed "
+                   f"{spent:.1f} s; whole-workload time {t_full:.0f} s extrapolated by exact "
+                   f"key counts"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--dense-steps", type=int, default=1)
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the Delta Attention path of this library runs "
+              "on a single MI355X (heads would shard across GPUs with no communication); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2505_11254_amd import HEADLINE, WORKLOADS, binding
+    from paper_2505_11254_amd.inputs import generate
+
+    wl = WORKLOADS[args.workload or HEADLINE]
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    binding.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"workload {wl.name}: {wl.describe()}")
+
+    q, k, v, cu = generate(wl, device=dev)
+    kw = dict(B=wl.B) if wl.fixed_length else dict(cu_seqlens=cu, max_seqlen=wl.max_seqlen)
+    out = torch.empty_like(q)
+    ws_bytes = binding.workspace_bytes(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    cu_arg = None if wl.fixed_length else cu
+    pkw = dict(window=wl.window, n_sink=wl.n_sink, gamma=wl.gamma, B=wl.B, cu_seqlens=cu_arg,
+               max_seqlen=wl.max_seqlen)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(evs=None):
+        # the three kernels of one Delta Attention prefill, events between them
+        # recorded on the stream they are launched on
+        if evs is not None:
+            evs[0].record(stream)
+        binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_SPARSE, **pkw)
+        if evs is not None:
+            evs[1].record(stream)
+        binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_DENSE_ROWS, **pkw)
+        if evs is not None:
+            evs[2].record(stream)
+        binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_CORRECT, **pkw)
+        if evs is not None:
+            evs[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps)")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for s_ in range(args.steps):
+        step(evs[s_])
+    end.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    ms_total = start.elapsed_time(end)
+    ms_per_step = ms_total / args.steps
+    k_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps for i in range(3)]
+    log(f"delta path: {ms_per_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); "
+        f"sparse {k_ms[0]:.3f} ms, strided dense rows {k_ms[1]:.3f} ms, "
+        f"delta epilogue {k_ms[2]:.3f} ms")
+
+    T = wl.total_tokens
+    sp_pairs, dr_pairs, dc_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
+    fl = lambda pairs: 4.0 * wl.d * wl.Hq * pairs
+    flops = {"sparse": fl(sp_pairs), "dense_rows": fl(dr_pairs), "dense_causal": fl(dc_pairs)}
+
+    # dense causal baseline (the in-house quadratic kernel)
+    dense_ms = None
+    if not args.no_dense:
+        del ws
+        out_d = torch.empty_like(q)
+        tiny = generate(WORKLOADS["tiny_n1024_d64"], device=dev)
+        binding.dense_causal_attn_prefill(*tiny[:3])  # load the code object
+        torch.cuda.synchronize()
+        de0 = torch.cuda.Event(enable_timing=True)
+        de1 = torch.cuda.Event(enable_timing=True)
+        de0.record(stream)
+        for _ in range(args.dense_steps):
+            binding.dense_causal_attn_prefill(q, k, v, out=out_d, **kw)
+        de1.record(stream)
+        torch.cuda.synchronize()
+        dense_ms = de0.elapsed_time(de1) / args.dense_steps
+        log(f"dense causal: {dense_ms:.1f} ms ({flops['dense_causal'] / dense_ms / 1e9:.1f} "
+            f"TFLOP/s useful)")
+        del out_d
+
+    per_kernel = {
+        "sparse_window": {"ms": k_ms[0], "useful_tflops": flops["sparse"] / k_ms[0] / 1e9},
+        "strided_dense_rows": {"ms": k_ms[1],
+                               "useful_tflops": flops["dense_rows"] / k_ms[1] / 1e9},
+        "delta_epilogue": {"ms": k_ms[2], "gbs": epilogue_bytes(wl) / k_ms[2] / 1e6,
+                           "hbm_frac": epilogue_bytes(wl) / k_ms[2] / 1e6 / PEAK_HBM_GBS},
+    }
+    if dense_ms is not None:
+        per_kernel["dense_causal"] = {"ms": dense_ms,
+                                      "useful_tflops": flops["dense_causal"] / dense_ms / 1e9}
+    dom = max(("sparse_window", "strided_dense_rows"), key=lambda n: per_kernel[n]["ms"])
+    dom_flops = flops["sparse"] if dom == "sparse_window" else flops["dense_rows"]
+    achieved = dom_flops / per_kernel[dom]["ms"] / 1e9
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": load_traffic(dom, wl.name)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a bounded sample of the workload ...")
+        cpu = cpu_baseline(wl, q, k, v)
+        log(f"cpu baseline: {cpu}")
+
+    value = T / (ms_per_step / 1e3)
+    rec = {
+        "metric": "delta_prefill_tokens_per_s_per_layer",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": dict(wl.describe(), parallelism="single_gpu"),
+        "speedup_vs_dense_causal": round(dense_ms / ms_per_step, 2) if dense_ms else None,
+        "dense_causal_ms": round(dense_ms, 3) if dense_ms else None,
+        "kernels": {n: {kk: round(vv, 4) for kk, vv in d_.items()} for n, d_ in per_kernel.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -78,6 +78,33 @@ da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v,
                                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The steps of Algorithm 1 one at a time, for measuring each kernel on its
+ * own.  `steps` is a non-empty subset of the bits below; the steps it names
+ * run in this order, on `stream`, with the same buffers:
+ *   DA_STEP_SPARSE      step 1: A*V for every row into `out`, plus an fp32 copy
+ *                       of the anchor rows in the workspace;
+ *   DA_STEP_DENSE_ROWS  steps 2-3: A~V at the anchors (Eq. 4) and at the dense
+ *                       tail rows, as key-chunk partial results in the workspace;
+ *   DA_STEP_CORRECT     steps 4-5 (Eq. 6): merge the partials, form Delta and
+ *                       add it to the gamma rows of each group in `out`.
+ * Calls with DA_STEP_SPARSE, then DA_STEP_DENSE_ROWS, then DA_STEP_CORRECT
+ * (or one call with DA_STEP_ALL) equal one delta_attn_prefill[_varlen] call.
+ * A later step reads what earlier calls left in `out` and the workspace.
+ * cu_seqlens may be NULL: then B sequences of max_seqlen tokens each.
+ * Other arguments and errors as delta_attn_prefill_varlen; a `steps` value
+ * outside 1..7 gives DA_ERR_PARAM.
+ */
+#define DA_STEP_SPARSE 1u
+#define DA_STEP_DENSE_ROWS 2u
+#define DA_STEP_CORRECT 4u
+#define DA_STEP_ALL 7u
+da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, void* out,
+                                   const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                   int Hkv, int d, int window, int n_sink, int gamma,
+                                   void* workspace, size_t workspace_bytes, void* stream,
+                                   unsigned steps);
+
+/*
  * Sparse attention alone (f*, StreamingLLM sink + window; the first step of
  * Algorithm 1): out_i = (A*V)_i for every row.  Needs no workspace.
  */

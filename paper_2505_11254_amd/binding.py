@@ -21,10 +21,11 @@ LIB_PATH = os.path.join(_HERE, "libdelta_attn.so")
 STATUS = {0: "DA_OK", 1: "DA_ERR_NULL", 2: "DA_ERR_SHAPE", 3: "DA_ERR_PARAM",
           4: "DA_ERR_UNSUPPORTED", 5: "DA_ERR_ALIGN", 6: "DA_ERR_WORKSPACE", 7: "DA_ERR_HIP"}
 
-# C entry points and their argument types: p = pointer, i = int, z = size_t
+# C entry points and their argument types: p = pointer, i = int, z = size_t, u = unsigned
 SIGNATURES = {
     "delta_attn_prefill": "ppppiiiiiiiipzp",
     "delta_attn_prefill_varlen": "pppppiiiiiiiipzp",
+    "delta_attn_prefill_steps": "pppppiiiiiiiipzpu",
     "sparse_attn_prefill": "ppppiiiiiiip",
     "sparse_attn_prefill_varlen": "pppppiiiiiiip",
     "dense_causal_attn_prefill": "ppppiiiiip",
@@ -54,7 +55,8 @@ def load_library(path: str = LIB_PATH):
         raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
                            "(hipcc for gfx950); there is no fallback implementation")
     lib = ctypes.CDLL(path)
-    codes = {"p": ctypes.c_void_p, "i": ctypes.c_int, "z": ctypes.c_size_t}
+    codes = {"p": ctypes.c_void_p, "i": ctypes.c_int, "z": ctypes.c_size_t,
+             "u": ctypes.c_uint}
     for name, sig in SIGNATURES.items():
         f = getattr(lib, name)
         f.argtypes = [codes[c] for c in sig]
@@ -127,6 +129,20 @@ def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=Non
         _call("delta_attn_prefill_varlen", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
               _ptr(cu_seqlens), B_, N, Hq, Hkv, d, window, n_sink, gamma, _ptr(workspace),
               wsz, st)
+    return out
+
+
+STEP_SPARSE, STEP_DENSE_ROWS, STEP_CORRECT, STEP_ALL = 1, 2, 4, 7
+
+
+def delta_attn_prefill_steps(q, k, v, out, workspace, steps, *, window, n_sink, gamma, B=None,
+                             cu_seqlens=None, max_seqlen=None, stream=None):
+    """Run the given steps of Algorithm 1 (bit mask of STEP_*) on existing buffers."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    wsz = workspace.numel() * workspace.element_size()
+    _call("delta_attn_prefill_steps", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(cu_seqlens),
+          B_, N, Hq, Hkv, d, window, n_sink, gamma, _ptr(workspace), wsz,
+          _stream(q.device, stream), steps)
     return out
 
 

@@ -152,9 +152,11 @@ da_status run_plain(const Problem& P, bool sparse, void* stream) {
   return DA_OK;
 }
 
-da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, void* stream) {
+da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, void* stream,
+                    unsigned steps) {
   da_status st = validate(P, true, true);
   if (st != DA_OK) return st;
+  if (steps < 1u || steps > DA_STEP_ALL) return DA_ERR_PARAM;
   Plan plan;
   if (!make_plan(P.B, P.N, P.Hq, P.Hkv, P.d, P.gamma, &plan)) return DA_ERR_SHAPE;
   if (!workspace || workspace_bytes < plan.bytes) return DA_ERR_WORKSPACE;
@@ -182,17 +184,24 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   a.chunk = plan.chunk;
   hipStream_t s = (hipStream_t)stream;
 
+  hipError_t e = hipSuccess;
   // Step 1: sparse attention for every row (+ fp32 copy at anchors).
-  hipError_t e = launch_sparse(a, s);
-  if (e != hipSuccess) return fail_hip(e);
-  // Step 2: dense attention at anchors and tail rows, key axis split in chunks.
-  Args ar = a;
-  ar.n_rtiles = (plan.nR_max + kRowsPerWave * a.ppw - 1) / (kRowsPerWave * a.ppw);
-  e = launch_dense_rows(ar, s);
-  if (e != hipSuccess) return fail_hip(e);
-  // Step 3: merge, Delta, broadcast-add in place.
-  e = launch_delta_epilogue(a, s);
-  if (e != hipSuccess) return fail_hip(e);
+  if (steps & DA_STEP_SPARSE) {
+    e = launch_sparse(a, s);
+    if (e != hipSuccess) return fail_hip(e);
+  }
+  // Steps 2-3: dense attention at anchors and tail rows, key axis split in chunks.
+  if (steps & DA_STEP_DENSE_ROWS) {
+    Args ar = a;
+    ar.n_rtiles = (plan.nR_max + kRowsPerWave * a.ppw - 1) / (kRowsPerWave * a.ppw);
+    e = launch_dense_rows(ar, s);
+    if (e != hipSuccess) return fail_hip(e);
+  }
+  // Steps 4-5: merge, Delta, broadcast-add in place.
+  if (steps & DA_STEP_CORRECT) {
+    e = launch_delta_epilogue(a, s);
+    if (e != hipSuccess) return fail_hip(e);
+  }
   return DA_OK;
 }
 
@@ -207,7 +216,7 @@ da_status delta_attn_prefill(const void* q, const void* k, const void* v, void* 
                              int Hq, int Hkv, int N, int d, int window, int n_sink, int gamma,
                              void* workspace, size_t workspace_bytes, void* stream) {
   Problem P{q, k, v, out, nullptr, B, N, Hq, Hkv, d, window, n_sink, gamma};
-  return da::run_delta(P, workspace, workspace_bytes, stream);
+  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL);
 }
 
 da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v, void* out,
@@ -216,7 +225,16 @@ da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v,
                                     void* workspace, size_t workspace_bytes, void* stream) {
   if (!cu_seqlens) return DA_ERR_NULL;
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
-  return da::run_delta(P, workspace, workspace_bytes, stream);
+  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL);
+}
+
+da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, void* out,
+                                   const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                   int Hkv, int d, int window, int n_sink, int gamma,
+                                   void* workspace, size_t workspace_bytes, void* stream,
+                                   unsigned steps) {
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
+  return da::run_delta(P, workspace, workspace_bytes, stream, steps);
 }
 
 da_status sparse_attn_prefill(const void* q, const void* k, const void* v, void* out, int B,
