@@ -159,44 +159,62 @@ void attn_kernel(Args a) {
                                                     a.gamma) : -1;
 
   // Q fragments: lane holds dims kk*16 + half*8 .. +8 of its row, for every kk.
+  // Rows past the end of the block load row R1-1's query (a valid row) and are
+  // never written, so no load sits behind a branch.
   bf16x8 qf[D / 16];
   {
-    const int64_t qrow = ((sq.base + (row_valid ? my_pos : 0)) * a.Hq + h) * (int64_t)D;
-    const uint16_t* qp = a.q + qrow + half * 8;
+    const int pos_ld = row_valid ? my_pos : row_pos<MODE>(R1 - 1, nA, Lc, a.gamma);
+    const uint16_t* qp = a.q + ((sq.base + pos_ld) * a.Hq + h) * (int64_t)D + half * 8;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      u32x4 raw = row_valid ? *(const u32x4*)(qp + kk * 16) : u32x4{0u, 0u, 0u, 0u};
-      qf[kk] = __builtin_bit_cast(bf16x8, raw);
-    }
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + kk * 16);
+    // retire the Q loads here (vmcnt(0)): the main loop's MFMAs read qf every
+    // iteration and must not wait behind the prefetch loads issued in it
+    __builtin_amdgcn_s_waitcnt(0x0F70);
   }
 
   const int64_t kv_stride = (int64_t)a.Hkv * D;  // elements between consecutive keys
   const uint16_t* kbase = a.k + (sq.base * a.Hkv + g) * (int64_t)D;
   const uint16_t* vbase = a.v + (sq.base * a.Hkv + g) * (int64_t)D;
 
+  // Per-thread byte offsets of the tile loads, relative to the tile's first key.
+  // K: thread u loads 16 bytes (8 dims) of key u/(D/8).  V: the 16 lanes of a
+  // group take the 16 four-key groups of the tile and the group index picks 8
+  // dims, so each lane loads 4 keys x 8 dims and writes them transposed.
+  const int vkg = tid & 15;  // 4-key group of the tile
+  const int vdc = tid >> 4;  // 8-dim chunk
+  int koff[LD::kLoads];
+#pragma unroll
+  for (int i = 0; i < LD::kLoads; ++i) {
+    const int u = tid + i * kThreads;
+    koff[i] = (int)((u / (D / 8)) * kv_stride * 2 + (u % (D / 8)) * 16);
+  }
+  const int voff0 = (int)(vkg * 4 * kv_stride * 2 + vdc * 16);
+  const int vrow = (int)(kv_stride * 2);
+
   u32x4 kreg[LD::kLoads];
   u32x4 vreg[4];
 
   auto tile_at = [&](int it) { return it < n_a ? ta0 + it : tb0 + (it - n_a); };
 
-  // global -> registers: K as 16-byte row pieces, V as 4 keys x 8 dims per thread
+  // global -> registers through buffer descriptors re-based at the tile's
+  // first key; their range ends at the sequence end, so keys past it read as
+  // zero (every valid row masks them: they lie after its position).
   auto gload = [&](int tile) {
-    const int key0 = tile * kKeyTile;
+    const int64_t key0 = (int64_t)tile * kKeyTile;
+    const int64_t bytes = (L - key0) * kv_stride * 2;
+    const int nrec = (int)min(bytes, (int64_t)0x7fffffff);
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(kbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(vbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < LD::kLoads; ++i) {
-      const int u = tid + i * kThreads;
-      const int j = key0 + u / (D / 8);
-      const int ch = u % (D / 8);
-      kreg[i] = j < L ? *(const u32x4*)(kbase + j * kv_stride + ch * 8) : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < LD::kLoads; ++i)
+      kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, koff[i], 0, 0));
     if (tid < LD::vUnits) {
-      const int dc = tid % (D / 8);
-      const int kg = tid / (D / 8);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = key0 + kg * 4 + r;
-        vreg[r] = j < L ? *(const u32x4*)(vbase + j * kv_stride + dc * 8) : u32x4{0u, 0u, 0u, 0u};
-      }
+      for (int r = 0; r < 4; ++r)
+        vreg[r] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, voff0 + r * vrow, 0, 0));
     }
   };
 
@@ -204,7 +222,8 @@ void attn_kernel(Args a) {
   // gives a lane the 8 keys of its MFMA k-slots.  Inside each 16-key block the
   // key groups 4..7 and 8..11 swap places: lane half h then finds keys
   // {4h..4h+3, 8+4h..8+4h+3} contiguous, which is the order the S^T
-  // accumulator hands them over as P^T.
+  // accumulator hands them over as P^T.  The 16 lanes of a group write one
+  // V^T row (16 x 8 bytes), which keeps the writes free of bank conflicts.
   auto lds_store = [&](int buf) {
     uint16_t* ks = smem + buf * LD::stageElems;
     uint16_t* vs = ks + LD::kElems;
@@ -214,10 +233,8 @@ void attn_kernel(Args a) {
       *(u32x4*)(ks + (u / (D / 8)) * LD::kStride + (u % (D / 8)) * 8) = kreg[i];
     }
     if (tid < LD::vUnits) {
-      const int dc = tid % (D / 8);
-      const int kg = tid / (D / 8);
-      const int sb = kg & 3;
-      const int pg = (kg & ~3) | ((sb == 1) ? 2 : (sb == 2) ? 1 : sb);
+      const int sb = vkg & 3;
+      const int pg = (vkg & ~3) | ((sb == 1) ? 2 : (sb == 2) ? 1 : sb);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int w = e >> 1;
@@ -229,7 +246,7 @@ void attn_kernel(Args a) {
           lo = (vreg[0][w] & 0xffffu) | (vreg[1][w] << 16);
           hi = (vreg[2][w] & 0xffffu) | (vreg[3][w] << 16);
         }
-        *(u32x2*)(vs + (dc * 8 + e) * LD::vStride + pg * 4) = u32x2{lo, hi};
+        *(u32x2*)(vs + (vdc * 8 + e) * LD::vStride + pg * 4) = u32x2{lo, hi};
       }
     }
   };
@@ -286,14 +303,20 @@ void attn_kernel(Args a) {
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m, mx);
-    const bool none = (m_new == -INFINITY);
-    const float alpha = none ? 1.f : fast_exp2((m - m_new) * scale);
-    const float mc = none ? 0.f : m_new * scale;
-    m = m_new;
-    l *= alpha;
+    // The reference max m only moves when a score exceeds it by more than
+    // 2^8 after exponentiation; otherwise P may reach 256 (harmless in fp32
+    // and bf16) and the rescale of O and l is skipped.  The result is the
+    // same: numerator and normaliser share the reference.
+    const bool grow = (mx - m) * scale > 8.f;
+    if (__any(grow)) {
+      const float m_new = fmaxf(m, mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2((m - m_new) * scale);
+      m = m_new;
+      l *= alpha;
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+    }
+    const float mc = (m == -INFINITY) ? 0.f : m * scale;
     f32x16 p0, p1;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -318,10 +341,9 @@ void attn_kernel(Args a) {
   };
 
   // ---- double-buffered main loop: prefetch tile it+1 while computing tile it
-  if (n_iter > 0) {
-    gload(tile_at(0));
-    lds_store(0);
-  }
+  // (every block that reaches this point has n_iter >= 1)
+  gload(tile_at(0));
+  lds_store(0);
   __syncthreads();
   for (int it = 0; it < n_iter; ++it) {
     const int buf = it & 1;
