@@ -13,8 +13,9 @@
 //   S^T[key][row] = K Q^T   with v_mfma_f32_32x32x16_bf16: A = K rows from
 //                           LDS, B = the wave's Q rows held in registers;
 //   P^T = exp2(S^T * log2(e)/sqrt(d) - m)   online softmax in fp32;
-//   O^T[dim][row] += V^T P^T  A = V^T from LDS (stored transposed), B = P^T
-//                           taken straight from the S^T accumulator registers.
+//   O^T[dim][row] += V^T P^T  A = V^T read from the row-major V tile with
+//                           gfx950's transposing LDS reads, B = P^T taken
+//                           straight from the S^T accumulator registers.
 // With this orientation a lane owns one query row in every accumulator
 // (lane % 32 = row), so the row max, the normaliser and the rescale of O
 // stay in the lane apart from one exchange with lane ^ 32, and P never goes
@@ -36,17 +37,26 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 enum Mode { kSparse = 0, kDense = 1, kDenseRows = 2 };
 
-// LDS layout of one pipeline stage (bf16 elements).  Rows are padded by 16
-// bytes so the 16-byte fragment reads of 32 consecutive rows hit distinct banks.
+// LDS layout of one pipeline stage (bf16 elements): K and V tiles of 64 keys,
+// both row-major [key][dim] with unpadded rows of 2*D bytes.  Tiles arrive by
+// LDS DMA, which writes 1 KB contiguous per wave instruction, so bank
+// conflicts are avoided by XOR-swizzling the 16-byte chunks of each row
+// instead of padding it:
+//   K: chunk c of key row r sits at c ^ kswz(r), which spreads the 16-byte
+//      operand reads of 16 consecutive keys over all banks;
+//   V: chunk c of key row r sits at c ^ vswz(r), which spreads the transposing
+//      8-byte reads (four keys x sixteen dims per 16-lane group).
 template <int D>
 struct Lds {
-  static constexpr int kStride = D + 8;              // K tile row: one key, D dims
-  static constexpr int vStride = kKeyTile + 8;       // V^T tile row: one dim, 64 keys
-  static constexpr int kElems = kKeyTile * kStride;
-  static constexpr int vElems = D * vStride;
+  static constexpr int kElems = kKeyTile * D;
+  static constexpr int vElems = kKeyTile * D;
   static constexpr int stageElems = kElems + vElems;
-  static constexpr int kLoads = kKeyTile * D / 8 / kThreads;  // 16-byte K loads per thread
-  static constexpr int vUnits = (kKeyTile / 4) * (D / 8);      // (4 keys x 8 dims) V units
+  static constexpr int kRegions = kKeyTile * D * 2 / 1024;  // 1 KB DMA regions per tile
+  static constexpr int kRegionsPerWave = kRegions / kWavesPerBlock;
+  __device__ static constexpr int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+  __device__ static constexpr int vswz(int r) {
+    return D == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
+  }
 };
 
 struct Seq {
@@ -77,6 +87,27 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+// 16 bytes per lane from a buffer into LDS at lds + 16*lane (LDS DMA).  The
+// builtin exists only for the GPU target; in the host pass of the kernel
+// templates it would silently drop the kernels' host stubs, so the host pass
+// sees an empty body.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint16_t* lds, int voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16,
+                                           voff, 0, 0, 0);
+#endif
+}
+
+// ds_read_b64_tr_b16: inside each group of 16 lanes, lane i receives element
+// k (k = 0..3) of the 8-byte row read by lane 4k + i/4, at position i%4.
+__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (i16x4 __attribute__((address_space(3)))*)(p));
+}
 
 // Row index -> position of that row inside its sequence.  In the strided
 // dense-row mode row r < nA is anchor r*gamma, later rows are tail rows.
@@ -176,30 +207,25 @@ void attn_kernel(Args a) {
   const uint16_t* kbase = a.k + (sq.base * a.Hkv + g) * (int64_t)D;
   const uint16_t* vbase = a.v + (sq.base * a.Hkv + g) * (int64_t)D;
 
-  // Per-thread byte offsets of the tile loads, relative to the tile's first key.
-  // K: thread u loads 16 bytes (8 dims) of key u/(D/8).  V: the 16 lanes of a
-  // group take the 16 four-key groups of the tile and the group index picks 8
-  // dims, so each lane loads 4 keys x 8 dims and writes them transposed.
-  const int vkg = tid & 15;  // 4-key group of the tile
-  const int vdc = tid >> 4;  // 8-dim chunk
-  int koff[LD::kLoads];
+  // ---- tile loads by LDS DMA.  buffer_load_dwordx4 ... lds writes 16 bytes per
+  // lane at M0 + 16*lane, so one instruction fills one 1 KB region of a tile.
+  // Wave w fills regions w*RPW .. w*RPW+RPW-1 of both tiles; lane l of region
+  // n lands on key row r = (1024n + 16l) / 2D at physical chunk pc and so
+  // fetches logical chunk pc ^ swizzle(r) of that key.  The descriptors are
+  // re-based at the tile's first key and end at the sequence end: keys past it
+  // read as zero (and every valid row masks them).
+  constexpr int RPW = LD::kRegionsPerWave;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  int dma_koff[RPW], dma_voff[RPW];
 #pragma unroll
-  for (int i = 0; i < LD::kLoads; ++i) {
-    const int u = tid + i * kThreads;
-    koff[i] = (int)((u / (D / 8)) * kv_stride * 2 + (u % (D / 8)) * 16);
+  for (int i = 0; i < RPW; ++i) {
+    const int byte = (wave_s * RPW + i) * 1024 + 16 * lane;
+    const int r = byte / (2 * D);
+    const int pc = (byte % (2 * D)) / 16;
+    dma_koff[i] = (int)(r * kv_stride * 2) + (pc ^ LD::kswz(r)) * 16;
+    dma_voff[i] = (int)(r * kv_stride * 2) + (pc ^ LD::vswz(r)) * 16;
   }
-  const int voff0 = (int)(vkg * 4 * kv_stride * 2 + vdc * 16);
-  const int vrow = (int)(kv_stride * 2);
-
-  u32x4 kreg[LD::kLoads];
-  u32x4 vreg[4];
-
-  auto tile_at = [&](int it) { return it < n_a ? ta0 + it : tb0 + (it - n_a); };
-
-  // global -> registers through buffer descriptors re-based at the tile's
-  // first key; their range ends at the sequence end, so keys past it read as
-  // zero (every valid row masks them: they lie after its position).
-  auto gload = [&](int tile) {
+  auto dma = [&](int tile, int stage) {
     const int64_t key0 = (int64_t)tile * kKeyTile;
     const int64_t bytes = (L - key0) * kv_stride * 2;
     const int nrec = (int)min(bytes, (int64_t)0x7fffffff);
@@ -207,49 +233,33 @@ void attn_kernel(Args a) {
         (void*)(kbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
     const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(vbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
+    uint16_t* ks = smem + stage * LD::stageElems;
+    uint16_t* vs = ks + LD::kElems;
 #pragma unroll
-    for (int i = 0; i < LD::kLoads; ++i)
-      kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, koff[i], 0, 0));
-    if (tid < LD::vUnits) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        vreg[r] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, voff0 + r * vrow, 0, 0));
+    for (int i = 0; i < RPW; ++i) {
+      const int region = (wave_s * RPW + i) * 512;  // in bf16 elements
+      dma16(kr, ks + region, dma_koff[i]);
+      dma16(vr, vs + region, dma_voff[i]);
     }
   };
 
-  // registers -> LDS.  V is transposed to V^T[dim][key] so one 16-byte read
-  // gives a lane the 8 keys of its MFMA k-slots.  Inside each 16-key block the
-  // key groups 4..7 and 8..11 swap places: lane half h then finds keys
-  // {4h..4h+3, 8+4h..8+4h+3} contiguous, which is the order the S^T
-  // accumulator hands them over as P^T.  The 16 lanes of a group write one
-  // V^T row (16 x 8 bytes), which keeps the writes free of bank conflicts.
-  auto lds_store = [&](int buf) {
-    uint16_t* ks = smem + buf * LD::stageElems;
-    uint16_t* vs = ks + LD::kElems;
+  // Per-lane LDS read offsets (elements, stage 0).  K operand (nb, kk): key row
+  // 32nb + col, logical chunk 2kk + half.  V^T operand (t, mb): transposing
+  // reads where, inside each 16-lane group, lane 4k+m points at key
+  // 16t + 4h + k (and +8 for the second read) and dims 32mb + 16*g1 + 4m.
+  const int ksw = LD::kswz(col);
+  int kread[D / 16];
 #pragma unroll
-    for (int i = 0; i < LD::kLoads; ++i) {
-      const int u = tid + i * kThreads;
-      *(u32x4*)(ks + (u / (D / 8)) * LD::kStride + (u % (D / 8)) * 8) = kreg[i];
-    }
-    if (tid < LD::vUnits) {
-      const int sb = vkg & 3;
-      const int pg = (vkg & ~3) | ((sb == 1) ? 2 : (sb == 2) ? 1 : sb);
+  for (int kk = 0; kk < D / 16; ++kk) kread[kk] = col * D + (((2 * kk + half) ^ ksw) * 8);
+  const int tr_g1 = (lane >> 4) & 1, tr_k = (lane >> 2) & 3, tr_m = lane & 3;
+  const int vsw = LD::vswz(4 * half + tr_k);
+  int vread[D / 32];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int w = e >> 1;
-        uint32_t lo, hi;
-        if (e & 1) {
-          lo = (vreg[0][w] >> 16) | (vreg[1][w] & 0xffff0000u);
-          hi = (vreg[2][w] >> 16) | (vreg[3][w] & 0xffff0000u);
-        } else {
-          lo = (vreg[0][w] & 0xffffu) | (vreg[1][w] << 16);
-          hi = (vreg[2][w] & 0xffffu) | (vreg[3][w] << 16);
-        }
-        *(u32x2*)(vs + (vdc * 8 + e) * LD::vStride + pg * 4) = u32x2{lo, hi};
-      }
-    }
-  };
+  for (int mb = 0; mb < D / 32; ++mb)
+    vread[mb] = (4 * half + tr_k) * D + (((4 * mb + 2 * tr_g1 + (tr_m >> 1)) ^ vsw) * 8) +
+                (tr_m & 1) * 4;
+
+  auto tile_at = [&](int it) { return it < n_a ? ta0 + it : tb0 + (it - n_a); };
 
   // 0: no key of the tile is visible to any row of the wave; 1: every key is
   // visible to every row; 2: mixed, mask per element.
@@ -268,18 +278,19 @@ void attn_kernel(Args a) {
   f32x16 o[D / 32];
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
-  float m = -INFINITY;  // running max of raw scores (same in lanes l and l^32)
+  float m = -INFINITY;  // reference max of raw scores (same in lanes l and l^32)
   float l = 0.f;        // this lane's share of the softmax normaliser
   const float scale = a.scale_log2;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  auto compute = [&](int buf, int tile, bool masked) {
-    const uint16_t* ks = smem + buf * LD::stageElems;
+  auto compute = [&](const uint16_t* ks, int tile, bool masked) {
     const uint16_t* vs = ks + LD::kElems;
     f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
-      const bf16x8 ka = *(const bf16x8*)(ks + col * LD::kStride + kk * 16 + half * 8);
-      const bf16x8 kb = *(const bf16x8*)(ks + (32 + col) * LD::kStride + kk * 16 + half * 8);
+      const bf16x8 ka = *(const bf16x8*)(ks + kread[kk]);
+      const bf16x8 kb = *(const bf16x8*)(ks + kread[kk] + 32 * D);
       s0 = mfma32(ka, qf[kk], s0);
       s1 = mfma32(kb, qf[kk], s1);
     }
@@ -299,10 +310,22 @@ void attn_kernel(Args a) {
         s1[r] = ok1 ? s1[r] : -INFINITY;
       }
     }
-    float mx = fmaxf(s0[0], s1[0]);
+    // row max over the 32 scores of this lane (a tree of 3-input max), then
+    // across the lane pair l, l^32 that shares the row
+    float t3[11];
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    for (int r = 0; r < 5; ++r) t3[r] = fmaxf(s0[3 * r], fmaxf(s0[3 * r + 1], s0[3 * r + 2]));
+#pragma unroll
+    for (int r = 0; r < 5; ++r) t3[5 + r] = fmaxf(s1[3 * r], fmaxf(s1[3 * r + 1], s1[3 * r + 2]));
+    t3[10] = fmaxf(s0[15], s1[15]);
+    float mx = fmaxf(fmaxf(fmaxf(t3[0], t3[1]), fmaxf(t3[2], t3[3])),
+                     fmaxf(fmaxf(t3[4], t3[5]), fmaxf(t3[6], t3[7])));
+    mx = fmaxf(mx, fmaxf(t3[8], fmaxf(t3[9], t3[10])));
+    {
+      const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));
+    }
     // The reference max m only moves when a score exceeds it by more than
     // 2^8 after exponentiation; otherwise P may reach 256 (harmless in fp32
     // and bf16) and the rescale of O and l is skipped.  The result is the
@@ -322,9 +345,9 @@ void attn_kernel(Args a) {
     for (int r = 0; r < 16; ++r) {
       p0[r] = fast_exp2(fmaf(s0[r], scale, -mc));
       p1[r] = fast_exp2(fmaf(s1[r], scale, -mc));
-      l += p0[r] + p1[r];
     }
-    // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block t/2
+    // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block t/2.
+    // The normaliser sums the bf16 weights the MFMA multiplies (dot2 with 1,1).
     bf16x8 pf[4];
     pf[0] = __builtin_convertvector(p0.lo, bf16x8);
     pf[1] = __builtin_convertvector(p0.hi, bf16x8);
@@ -332,30 +355,47 @@ void attn_kernel(Args a) {
     pf[3] = __builtin_convertvector(p1.hi, bf16x8);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 0, 1), ones2, l, false);
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 2, 3), ones2, l, false);
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 4, 5), ones2, l, false);
+      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 6, 7), ones2, l, false);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
 #pragma unroll
       for (int mb = 0; mb < D / 32; ++mb) {
-        const bf16x8 va = *(const bf16x8*)(vs + (32 * mb + col) * LD::vStride + 16 * t + 8 * half);
-        o[mb] = mfma32(va, pf[t], o[mb]);
+        const i16x4 lo = lds_read_tr(vs + vread[mb] + (16 * t) * D);
+        const i16x4 hi = lds_read_tr(vs + vread[mb] + (16 * t + 8) * D);
+        const i16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        o[mb] = mfma32(__builtin_bit_cast(bf16x8, both), pf[t], o[mb]);
       }
     }
   };
 
-  // ---- double-buffered main loop: prefetch tile it+1 while computing tile it
-  // (every block that reaches this point has n_iter >= 1)
-  gload(tile_at(0));
-  lds_store(0);
+  // ---- main loop, one barrier per tile.  Step `it` waits for its own DMA of
+  // tile it, meets the other waves at the barrier (after which tile it is in
+  // LDS and nobody reads the other stage any more), starts the DMA of tile
+  // it+1 into the other stage, then computes tile it.  LDS starts zeroed so a
+  // key that the DMA leaves untouched is a finite value.
+  for (int i = tid; i < 2 * LD::stageElems / 8; i += kThreads)
+    *(u32x4*)(smem + 8 * i) = u32x4{0u, 0u, 0u, 0u};
   __syncthreads();
-  for (int it = 0; it < n_iter; ++it) {
-    const int buf = it & 1;
-    const int tile = tile_at(it);
-    if (it + 1 < n_iter) gload(tile_at(it + 1));
-    const int cls = classify(tile);
-    if (cls == 1)
-      compute(buf, tile, false);
-    else if (cls == 2)
-      compute(buf, tile, true);
-    if (it + 1 < n_iter) lds_store(buf ^ 1);
+  dma(tile_at(0), 0);
+  auto step = [&](int it, int stage) {
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's DMA of tile it
     __syncthreads();
+    if (it + 1 < n_iter) dma(tile_at(it + 1), stage ^ 1);
+    const int tile = tile_at(it);
+    const int cls = classify(tile);
+    const uint16_t* ks = smem + stage * LD::stageElems;
+    if (cls == 1)
+      compute(ks, tile, false);
+    else if (cls == 2)
+      compute(ks, tile, true);
+  };
+  for (int it = 0; it < n_iter; it += 2) {
+    step(it, 0);
+    if (it + 1 < n_iter) step(it + 1, 1);
   }
 
   // ---- epilogue: output register r of block mb is dim 32*mb + 8*(r/4) + 4*half + r%4
