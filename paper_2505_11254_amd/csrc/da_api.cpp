@@ -51,26 +51,21 @@ int heads_per_block(int G) {
 
 // Workspace of the Delta path.  Dense rows of a sequence of length L are the
 // floor(L/gamma) anchors plus the L mod gamma tail rows.  Their key axis is
-// split into nC chunks of `chunk` keys so that short sequences still give the
-// GPU enough workgroups; nC is chosen for about 16K (row tile x chunk) units
-// and capped so the partial results stay within 4 GiB.
+// split into nC chunks of `chunk` keys (at least 2048), up to 16 of them.
+// Workgroups that run at the same time then process one key chunk each in
+// step with their neighbours, which keeps them sharing that chunk's keys and
+// values in L2.  nC drops only when the partial results would pass 8 GiB.
 bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p) {
   if (B < 1 || max_seqlen < 1 || Hq < 1 || Hkv < 1 || gamma < 1 || (d != 64 && d != 128))
     return false;
   if (Hq % Hkv != 0) return false;
   const int64_t nA_max = max_seqlen / gamma;
   const int64_t nR_max = nA_max + (int64_t)((gamma - 1 < max_seqlen) ? gamma - 1 : max_seqlen);
-  const int hpw = heads_per_block(Hq / Hkv);
-  const int64_t rows_per_block = (int64_t)kRowsPerWave * (kWavesPerBlock / hpw);
-  const int64_t rtiles = (nR_max + rows_per_block - 1) / rows_per_block;
-  const int64_t units = (int64_t)B * (Hq / hpw) * rtiles;
-  int64_t nC = (16384 + units - 1) / units;
+  int64_t nC = (max_seqlen + kKeyTile * 32 - 1) / (kKeyTile * 32);  // >= 2048 keys each
   if (nC > 16) nC = 16;
-  const int64_t max_chunks = (max_seqlen + kKeyTile * 32 - 1) / (kKeyTile * 32);  // >= 2048 keys each
-  if (nC > max_chunks) nC = max_chunks;
   if (nC < 1) nC = 1;
   const int64_t per_chunk_bytes = (int64_t)B * Hq * nR_max * (d + 2) * 4;
-  const int64_t budget = (int64_t)4 << 30;
+  const int64_t budget = (int64_t)8 << 30;
   while (nC > 1 && per_chunk_bytes * nC > budget) --nC;
   int64_t chunk = (max_seqlen + nC - 1) / nC;
   chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
