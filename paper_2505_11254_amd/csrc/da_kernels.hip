@@ -140,7 +140,10 @@ void attn_kernel(Args a) {
   }
   const int hg = (int)(lid % a.n_hgroups);
   const int b = (int)(lid / a.n_hgroups);
-  if (MODE == kDense) rt = a.n_rtiles - 1 - rt;  // longest rows first
+  // Longest rows first: in the dense modes blocks dispatched together then have
+  // (nearly) the same number of key tiles, start on the same tile and stay in
+  // step, so they share each key/value tile in L2.
+  if (MODE != kSparse) rt = a.n_rtiles - 1 - rt;
 
   const Seq sq = seq_of(a, b);
   const int L = sq.L;
