@@ -5,7 +5,7 @@
 
 #include <atomic>
 
-#include "../../include/delta_attn.h"
+#include "delta_attn.h"
 #include "da_internal.hpp"
 
 namespace da {
@@ -43,10 +43,12 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 }  // namespace
 
+// Query heads of one GQA group that share an attention workgroup: the
+// largest power of two dividing G, at most kAttnWaves.
 int heads_per_block(int G) {
-  if (G % 4 == 0) return 4;
-  if (G % 2 == 0) return 2;
-  return 1;
+  int h = 1;
+  while (h * 2 <= kAttnWaves && G % (h * 2) == 0) h *= 2;
+  return h;
 }
 
 // Workspace of the Delta path.  Dense rows of a sequence of length L are the
@@ -102,7 +104,7 @@ da_status validate(const Problem& P, bool need_window, bool need_gamma) {
   // token indices and row-tile counts are 32-bit inside the kernels
   if (!P.cu && (int64_t)P.B * P.N > INT32_MAX) return DA_ERR_SHAPE;
   const int hpw = heads_per_block(P.Hq / P.Hkv);
-  const int64_t rows_per_block = (int64_t)kRowsPerWave * (kWavesPerBlock / hpw);
+  const int64_t rows_per_block = (int64_t)kRowsPerWave * (kAttnWaves / hpw);
   const int64_t blocks = (int64_t)P.B * (P.Hq / hpw) * ((P.N + rows_per_block - 1) / rows_per_block);
   if (blocks > INT32_MAX) return DA_ERR_SHAPE;
   if (!aligned16(P.q) || !aligned16(P.k) || !aligned16(P.v) || !aligned16(P.out))
@@ -128,7 +130,7 @@ Args base_args(const Problem& P) {
   a.gamma = P.gamma > 0 ? P.gamma : 1;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)P.d));
   a.hpw = heads_per_block(P.Hq / P.Hkv);
-  a.ppw = kWavesPerBlock / a.hpw;
+  a.ppw = kAttnWaves / a.hpw;
   a.n_hgroups = P.Hq / a.hpw;
   const int rows_per_block = kRowsPerWave * a.ppw;
   a.n_rtiles = (P.N + rows_per_block - 1) / rows_per_block;
@@ -158,7 +160,7 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   if (!aligned16(workspace)) return DA_ERR_ALIGN;
   {
     const int hpw = heads_per_block(P.Hq / P.Hkv);
-    const int64_t rows_per_block = (int64_t)kRowsPerWave * (kWavesPerBlock / hpw);
+    const int64_t rows_per_block = (int64_t)kRowsPerWave * (kAttnWaves / hpw);
     const int64_t rtiles = (plan.nR_max + rows_per_block - 1) / rows_per_block;
     if ((int64_t)P.B * (P.Hq / hpw) * plan.nC * rtiles > INT32_MAX) return DA_ERR_SHAPE;
     if ((int64_t)P.B * plan.nR_max * ((P.Hq + 8192 / P.d - 1) / (8192 / P.d)) > INT32_MAX)

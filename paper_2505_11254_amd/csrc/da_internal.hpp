@@ -12,8 +12,14 @@ namespace da {
 // Keys per tile of every attention kernel, and query rows per wavefront.
 constexpr int kKeyTile = 64;
 constexpr int kRowsPerWave = 32;
-constexpr int kWavesPerBlock = 4;
-constexpr int kThreads = 64 * kWavesPerBlock;
+// Attention workgroups: kAttnWaves wavefronts share every K/V tile, which
+// passes through a ring of kAttnStages LDS buffers (prefetch distance
+// kAttnStages - 1 tiles).
+constexpr int kAttnWaves = 8;
+constexpr int kAttnStages = 2;
+constexpr int kAttnThreads = 64 * kAttnWaves;
+// Delta epilogue workgroups.
+constexpr int kEpiThreads = 256;
 
 // Everything a kernel needs; passed by value as the kernel argument.
 struct Args {
@@ -28,7 +34,7 @@ struct Args {
   float scale_log2;   // log2(e) / sqrt(d): scores are exponentiated with exp2
 
   // Workgroup tiling of (query heads x rows): hpw heads of one kv group, each
-  // with ppw sub-tiles of 32 rows; hpw * ppw == kWavesPerBlock.
+  // with ppw sub-tiles of 32 rows; hpw * ppw == kAttnWaves.
   int hpw, ppw;
   int n_hgroups;      // Hq / hpw
   int n_rtiles;       // row tiles (of 32 * ppw rows) per (sequence, head group)

@@ -19,8 +19,8 @@
 // With this orientation a lane owns one query row in every accumulator
 // (lane % 32 = row), so the row max, the normaliser and the rescale of O
 // stay in the lane apart from one exchange with lane ^ 32, and P never goes
-// through LDS.  K/V tiles are double-buffered in LDS; each workgroup of four
-// waves shares every K/V tile between the query heads of one GQA group.
+// through LDS.  K/V tiles go through a ring of LDS buffers; the waves of a
+// workgroup share every K/V tile between the query heads of one GQA group.
 #include "da_internal.hpp"
 
 #include <math.h>
@@ -52,7 +52,7 @@ struct Lds {
   static constexpr int vElems = kKeyTile * D;
   static constexpr int stageElems = kElems + vElems;
   static constexpr int kRegions = kKeyTile * D * 2 / 1024;  // 1 KB DMA regions per tile
-  static constexpr int kRegionsPerWave = kRegions / kWavesPerBlock;
+  static constexpr int kRegionsPerWave = kRegions / kAttnWaves;
   __device__ static constexpr int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
   __device__ static constexpr int vswz(int r) {
     return D == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
@@ -118,10 +118,11 @@ __device__ __forceinline__ int row_pos(int r, int nA, int Lc, int gamma) {
 }
 
 template <int D, int MODE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(Args a) {
   using LD = Lds<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * LD::stageElems];
+  constexpr int NS = kAttnStages;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[NS * LD::stageElems];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -375,30 +376,36 @@ void attn_kernel(Args a) {
     }
   };
 
-  // ---- main loop, one barrier per tile.  Step `it` waits for its own DMA of
-  // tile it, meets the other waves at the barrier (after which tile it is in
-  // LDS and nobody reads the other stage any more), starts the DMA of tile
-  // it+1 into the other stage, then computes tile it.  LDS starts zeroed so a
-  // key that the DMA leaves untouched is a finite value.
-  for (int i = tid; i < 2 * LD::stageElems / 8; i += kThreads)
+  // ---- main loop over a ring of NS LDS stages, one barrier per tile.  Step
+  // `it` waits until this wave's DMA of tile it has landed (later tiles may
+  // still be in flight), meets the other waves at the barrier (after which
+  // tile it is in LDS for everyone and nobody reads stage (it-1) % NS any
+  // more), starts the DMA of tile it+NS-1 into that stage, then computes
+  // tile it.  LDS starts zeroed so a key the DMA leaves untouched is finite.
+  for (int i = tid; i < NS * LD::stageElems / 8; i += kAttnThreads)
     *(u32x4*)(smem + 8 * i) = u32x4{0u, 0u, 0u, 0u};
   __syncthreads();
-  dma(tile_at(0), 0);
-  auto step = [&](int it, int stage) {
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's DMA of tile it
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < n_iter) dma(tile_at(p), p);
+  constexpr int kLoadsPerTile = 2 * RPW;  // vmcnt entries one tile's DMA adds per wave
+  for (int it = 0; it < n_iter; ++it) {
+    const int ahead = min(NS - 2, n_iter - 1 - it);  // later tiles already in flight
+    if (NS >= 4 && ahead >= 2)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kLoadsPerTile) & 15) | (((2 * kLoadsPerTile) >> 4) << 14));
+    else if (NS >= 3 && ahead >= 1)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (kLoadsPerTile & 15) | ((kLoadsPerTile >> 4) << 14));
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
-    if (it + 1 < n_iter) dma(tile_at(it + 1), stage ^ 1);
+    if (it + NS - 1 < n_iter) dma(tile_at(it + NS - 1), (it + NS - 1) % NS);
     const int tile = tile_at(it);
     const int cls = classify(tile);
-    const uint16_t* ks = smem + stage * LD::stageElems;
+    const uint16_t* ks = smem + (it % NS) * LD::stageElems;
     if (cls == 1)
       compute(ks, tile, false);
     else if (cls == 2)
       compute(ks, tile, true);
-  };
-  for (int it = 0; it < n_iter; it += 2) {
-    step(it, 0);
-    if (it + 1 < n_iter) step(it + 1, 1);
   }
 
   // ---- epilogue: output register r of block mb is dim 32*mb + 8*(r/4) + 4*half + r%4
@@ -450,7 +457,7 @@ void attn_kernel(Args a) {
 // An anchor with a < n_sink + window sees all keys 0..a in its sparse set, so
 // its Delta is exactly zero and the block leaves its rows untouched.
 template <int D>
-__global__ __launch_bounds__(kThreads) void delta_epilogue_kernel(Args a) {
+__global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
   __shared__ float delta[8192];  // [head in range][D]
   const int tid = threadIdx.x;
   int64_t lid = blockIdx.x;
@@ -477,7 +484,7 @@ __global__ __launch_bounds__(kThreads) void delta_epilogue_kernel(Args a) {
   constexpr int DC = D / 8;
   typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
-  for (int idx = tid; idx < nh * DC; idx += kThreads) {
+  for (int idx = tid; idx < nh * DC; idx += kEpiThreads) {
     const int hh = idx / DC, dc = idx % DC;
     const int h = h0 + hh;
     const int64_t slot0 = (((int64_t)b * a.Hq + h) * a.nR_max + r) * a.nC;
@@ -507,7 +514,7 @@ __global__ __launch_bounds__(kThreads) void delta_epilogue_kernel(Args a) {
   // rows pos+1 .. pos+gamma-1 for heads [h0, h1): nh*D contiguous values per row
   const int per_row = nh * DC;
   const int64_t total = (int64_t)(a.gamma - 1) * per_row;
-  for (int64_t u = tid; u < total; u += kThreads) {
+  for (int64_t u = tid; u < total; u += kEpiThreads) {
     const int i = (int)(u / per_row);
     const int rem = (int)(u % per_row);
     const int hh = rem / DC, dc = rem % DC;
@@ -522,9 +529,9 @@ template <int MODE>
 hipError_t launch_attn(const Args& a, hipStream_t s, int64_t nblocks) {
   if (nblocks <= 0) return hipSuccess;
   if (a.d == 128)
-    hipLaunchKernelGGL((attn_kernel<128, MODE>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((attn_kernel<128, MODE>), dim3((unsigned)nblocks), dim3(kAttnThreads), 0, s, a);
   else
-    hipLaunchKernelGGL((attn_kernel<64, MODE>), dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((attn_kernel<64, MODE>), dim3((unsigned)nblocks), dim3(kAttnThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -547,9 +554,9 @@ hipError_t launch_delta_epilogue(const Args& a, hipStream_t s) {
   const int64_t nblocks = (int64_t)a.B * a.nR_max * n_hc;
   if (nblocks <= 0) return hipSuccess;
   if (a.d == 128)
-    hipLaunchKernelGGL(delta_epilogue_kernel<128>, dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(delta_epilogue_kernel<128>, dim3((unsigned)nblocks), dim3(kEpiThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(delta_epilogue_kernel<64>, dim3((unsigned)nblocks), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(delta_epilogue_kernel<64>, dim3((unsigned)nblocks), dim3(kEpiThreads), 0, s, a);
   return hipGetLastError();
 }
 
