@@ -148,6 +148,54 @@ def cpu_baseline(wl, q, k, v, target_s=12.0):
     }
 
 
+def time_sparse_only(binding, q, k, v, out, kw, wl, stream, steps):
+    import torch
+    binding.sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, out=out, **kw)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        binding.sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, out=out, **kw)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def gamma_sweep(args, wl, binding, q, k, v, kw, dev):
+    """Delta path vs sparse-only time for several gammas (same inputs)."""
+    import dataclasses
+
+    import torch
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(dev)
+    sparse_ms = time_sparse_only(binding, q, k, v, out, kw, wl, stream, args.steps)
+    for g in [int(x) for x in args.gamma_sweep.split(",")]:
+        w2 = dataclasses.replace(wl, gamma=g)
+        nbytes = binding.workspace_bytes(w2.B, w2.max_seqlen, w2.Hq, w2.Hkv, w2.d, g)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        run = lambda: binding.delta_attn_prefill(q, k, v, window=w2.window, n_sink=w2.n_sink,
+                                                 gamma=g, out=out, workspace=ws, **kw)
+        for _ in range(args.warmup):
+            run()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        sp, dr, dc = pair_counts(w2.seqlens, w2.window, w2.n_sink, g)
+        print(json.dumps({"workload": wl.name, "gamma": g, "delta_ms": round(ms, 4),
+                          "sparse_only_ms": round(sparse_ms, 4),
+                          "delta_overhead_vs_sparse": round(ms / sparse_ms, 4),
+                          "tokens_per_s": round(w2.total_tokens / ms * 1e3, 1),
+                          "strided_flop_fraction_of_dense": round(dr / dc, 5)}), flush=True)
+        del ws
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -157,6 +205,9 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=1)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gamma-sweep", default=None,
+                    help="comma-separated gammas: time the Delta path and the sparse-only "
+                         "kernel at each (one JSON line per gamma) instead of the main record")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB device buffer, a dispatch of known traffic "
                          "against which HBM byte counters are scaled")
@@ -190,6 +241,9 @@ def main():
 
     q, k, v, cu = generate(wl, device=dev)
     kw = dict(B=wl.B) if wl.fixed_length else dict(cu_seqlens=cu, max_seqlen=wl.max_seqlen)
+    if args.gamma_sweep:
+        gamma_sweep(args, wl, binding, q, k, v, kw, dev)
+        return
     out = torch.empty_like(q)
     ws_bytes = binding.workspace_bytes(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
@@ -235,6 +289,11 @@ def main():
     log(f"delta path: {ms_per_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); "
         f"sparse {k_ms[0]:.3f} ms, strided dense rows {k_ms[1]:.3f} ms, "
         f"delta epilogue {k_ms[2]:.3f} ms")
+
+    # sparse attention alone (f*, StreamingLLM) on the same inputs: the cost
+    # Delta adds on top of the sparse method it corrects
+    sparse_only_ms = time_sparse_only(binding, q, k, v, out, kw, wl, stream, args.steps)
+    log(f"sparse only: {sparse_only_ms:.3f} ms; delta overhead x{ms_per_step / sparse_only_ms:.3f}")
 
     T = wl.total_tokens
     sp_pairs, dr_pairs, dc_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
@@ -301,6 +360,8 @@ def main():
         "data": "synthetic",
         "config": dict(wl.describe(), parallelism="single_gpu"),
         "speedup_vs_dense_causal": round(dense_ms / ms_per_step, 2) if dense_ms else None,
+        "sparse_only_ms": round(sparse_only_ms, 4),
+        "delta_overhead_vs_sparse": round(ms_per_step / sparse_only_ms, 4),
         "dense_causal_ms": round(dense_ms, 3) if dense_ms else None,
         "kernels": {n: {kk: round(vv, 4) for kk, vv in d_.items()} for n, d_ in per_kernel.items()},
         "roofline": roofline,
