@@ -28,6 +28,9 @@ _LIB = os.path.join(_HERE, "libdelta_oracle.so")
 MODE_DENSE = 0
 MODE_SPARSE = 1
 
+# correction variants of step 5 (see dao_delta_attention_variant)
+CORR_DELTA, CORR_RECOMPUTE, CORR_INTERP, CORR_EMA, CORR_ABG = 0, 1, 2, 3, 4
+
 _lib = None
 
 
@@ -53,8 +56,11 @@ def _bind(path):
                                         i32, vp, vp, vp, i32]
     lib.dao_delta_attention_rows.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, i32,
                                              i32, i32, vp, i64, vp, vp, i32]
+    lib.dao_delta_attention_variant.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, i32,
+                                                i32, i32, i32, ctypes.c_double, ctypes.c_double,
+                                                ctypes.c_double, vp, i32]
     for f in (lib.dao_attention, lib.dao_attention_weights, lib.dao_delta_attention,
-              lib.dao_delta_attention_rows):
+              lib.dao_delta_attention_rows, lib.dao_delta_attention_variant):
         f.restype = ctypes.c_int
     lib.dao_max_threads.restype = ctypes.c_int
     lib.dao_max_threads.argtypes = []
@@ -196,6 +202,29 @@ class Oracle:
                                                 nthreads)
         _check(rc, "delta_attention_rows")
         return (out, dl) if return_delta else out
+
+
+def _variant(self, q, k, v, cu=None, *, window, n_sink, gamma, mode, params=(0.0, 0.0, 0.0),
+             nthreads=0):
+    """Algorithm 1 with the correction of step 5 chosen by ``mode`` (CORR_*)."""
+    P = _Problem(q, k, v, cu)
+    out = np.zeros((P.T, P.Hq, P.d))
+    p = list(params) + [0.0] * (3 - len(params))
+    rc = self._lib.dao_delta_attention_variant(*P.ptrs(), window, n_sink, gamma, mode,
+                                               float(p[0]), float(p[1]), float(p[2]),
+                                               out.ctypes.data, nthreads)
+    _check(rc, "delta_attention_variant")
+    return out
+
+
+Oracle.delta_attention_variant = _variant
+
+
+def delta_attention_variant(*args, **kw):
+    return Oracle().delta_attention_variant(*args, **kw)
+
+
+delta_attention_variant.__doc__ = _variant.__doc__
 
 
 def attention(*args, **kw):

@@ -395,6 +395,135 @@ int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in
   return err;
 }
 
+/*
+ * Correction variants (Sec. 3 "recompute", Eq. 5; interpolation appendix and
+ * its algorithm for the alpha-beta-gamma filter).  Steps 1-4 of Algorithm 1
+ * are as in dao_delta_attention: A*V for every row, A~V at the anchors,
+ * Delta_i = A~V_{a_i} - (A*V)_{a_i} for anchor a_i = i*gamma.  Step 5 adds a
+ * per-row correction c_r to (A*V)_r for r < L_c instead of repeat(Delta):
+ *   DAO_CORR_DELTA      c_r = Delta_{floor(r/gamma)}                  (Eq. 6)
+ *   DAO_CORR_RECOMPUTE  c_r = Delta_i if r = a_i, else 0               (Eq. 5)
+ *   DAO_CORR_INTERP     c_{a_i+k} = (1 - beta_k) Delta_i + beta_k Delta_{i+1},
+ *                       beta_k = k/(gamma-1) rising from 0 to 1 over the
+ *                       group (0 when gamma = 1); the last group has no
+ *                       successor and keeps Delta_i
+ *   DAO_CORR_EMA        D = repeat(Delta, gamma); E_r = (1-b) E_{r-1} + b D_r
+ *                       with E_{-1} = D_0, b = p0; c_r = E_r
+ *   DAO_CORR_ABG        alpha-beta-gamma filter over the sequence Delta_0..:
+ *                       o_0 = pos = Delta_0, vel = acc = 0; for i >= 1:
+ *                       pred = pos + vel + acc/2, vpred = vel + acc,
+ *                       res = Delta_i - pred, pos = pred + p0 res,
+ *                       vel = vpred + p1 res, acc = acc + p2 res, o_i = pos;
+ *                       c_r = o_{floor(r/gamma)}
+ * Rows past L_c take the dense result as in the other entry points.  Every
+ * operation is elementwise over the d channels.
+ */
+#define DAO_CORR_DELTA 0
+#define DAO_CORR_RECOMPUTE 1
+#define DAO_CORR_INTERP 2
+#define DAO_CORR_EMA 3
+#define DAO_CORR_ABG 4
+
+int dao_delta_attention_variant(const void* q, const void* k, const void* v, int in_bf16,
+                                const int64_t* cu, int B, int Hq, int Hkv, int d,
+                                int window, int n_sink, int gamma, int mode,
+                                double p0, double p1, double p2,
+                                double* out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  if (check_problem(&P) != DAO_OK || !out || gamma < 1) return DAO_ERR_ARG;
+  if (mode < DAO_CORR_DELTA || mode > DAO_CORR_ABG) return DAO_ERR_ARG;
+  const int64_t Lmax = max_len(&P);
+  int err = DAO_OK;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* sp = (double*)malloc(sizeof(double) * (size_t)((Lmax + 1) * d));
+    double* dl = (double*)malloc(sizeof(double) * (size_t)((Lmax / gamma + 1) * d));
+    double* cr = (double*)malloc(sizeof(double) * (size_t)d);
+    double* st = (double*)malloc(sizeof(double) * (size_t)(3 * d));
+#pragma omp for schedule(dynamic, 1) collapse(2)
+    for (int b = 0; b < B; ++b) {
+      for (int h = 0; h < Hq; ++h) {
+        if (!x || !sp || !dl || !cr || !st) {
+#pragma omp atomic write
+          err = DAO_ERR_NOMEM;
+          continue;
+        }
+        const int64_t L = cu[b + 1] - cu[b];
+        const int64_t nA = L / gamma;
+        const int64_t Lc = nA * gamma;
+        /* Step 1: A*V for every row of this sequence and head. */
+        for (int64_t i = 0; i < L; ++i)
+          attn_row(&P, DAO_MODE_SPARSE, b, h, i, sp + i * d, NULL, NULL, NULL, x);
+        /* Steps 2-4: Delta_i at every anchor a_i = i*gamma < Lc. */
+        for (int64_t i = 0; i < nA; ++i) {
+          attn_row(&P, DAO_MODE_DENSE, b, h, i * gamma, cr, NULL, NULL, NULL, x);
+          for (int c = 0; c < d; ++c) dl[i * d + c] = cr[c] - sp[i * gamma * d + c];
+        }
+        /* alpha-beta-gamma filter: replace Delta_i by the filtered o_i */
+        if (mode == DAO_CORR_ABG && nA > 0) {
+          double *pos = st, *vel = st + d, *acc = st + 2 * d;
+          for (int c = 0; c < d; ++c) { pos[c] = dl[c]; vel[c] = 0.0; acc[c] = 0.0; }
+          for (int64_t i = 1; i < nA; ++i) {
+            for (int c = 0; c < d; ++c) {
+              const double pred = pos[c] + vel[c] + 0.5 * acc[c];
+              const double vpred = vel[c] + acc[c];
+              const double res = dl[i * d + c] - pred;
+              pos[c] = pred + p0 * res;
+              vel[c] = vpred + p1 * res;
+              acc[c] = acc[c] + p2 * res;
+              dl[i * d + c] = pos[c];
+            }
+          }
+        }
+        /* Step 5 with the chosen correction, rows r < Lc */
+        double* ema = st; /* E_{r-1} */
+        if (mode == DAO_CORR_EMA && nA > 0)
+          for (int c = 0; c < d; ++c) ema[c] = dl[c];
+        for (int64_t r = 0; r < Lc; ++r) {
+          const int64_t i = r / gamma, kk = r % gamma;
+          for (int c = 0; c < d; ++c) {
+            double corr;
+            switch (mode) {
+              case DAO_CORR_RECOMPUTE:
+                corr = (kk == 0) ? dl[i * d + c] : 0.0;
+                break;
+              case DAO_CORR_INTERP: {
+                const double beta = (gamma > 1) ? (double)kk / (double)(gamma - 1) : 0.0;
+                const double next = (i + 1 < nA) ? dl[(i + 1) * d + c] : dl[i * d + c];
+                corr = (1.0 - beta) * dl[i * d + c] + beta * next;
+                break;
+              }
+              case DAO_CORR_EMA:
+                ema[c] = (1.0 - p0) * ema[c] + p0 * dl[i * d + c];
+                corr = ema[c];
+                break;
+              default: /* DELTA and the filtered ABG sequence */
+                corr = dl[i * d + c];
+            }
+            out[((cu[b] + r) * Hq + h) * (int64_t)d + c] = sp[r * d + c] + corr;
+          }
+        }
+        /* Tail rows: dense (implementation-details appendix). */
+        for (int64_t r = Lc; r < L; ++r)
+          attn_row(&P, DAO_MODE_DENSE, b, h, r, out + ((cu[b] + r) * Hq + h) * (int64_t)d,
+                   NULL, NULL, NULL, x);
+      }
+    }
+    free(x);
+    free(sp);
+    free(dl);
+    free(cr);
+    free(st);
+  }
+  return err;
+}
+
 /* Number of OpenMP threads a parallel region would use (1 without OpenMP). */
 int dao_max_threads(void) {
 #ifdef _OPENMP

@@ -75,3 +75,77 @@ def brute_parts(q, k, v, cu, window, n_sink, gamma):
 
 def brute_delta(q, k, v, cu, window, n_sink, gamma):
     return brute_parts(q, k, v, cu, window, n_sink, gamma)[0]
+
+
+# ---- correction variants (Sec. 3 "recompute", interpolation appendix) in matrix form ----
+
+def delta_rows(dense, sparse, L, gamma):
+    """Delta_i = dense - sparse at anchors a_i = i*gamma < floor(L/gamma)*gamma: [nA, d]."""
+    Lc = (L // gamma) * gamma
+    anchors = np.arange(0, Lc, gamma)
+    return dense[anchors] - sparse[anchors]
+
+
+def ema_matrix(n, b):
+    """E = W @ D + f * D_0 for E_r = (1-b) E_{r-1} + b D_r, E_{-1} = D_0 (closed form)."""
+    r = np.arange(n)[:, None]
+    s = np.arange(n)[None, :]
+    W = np.where(s <= r, b * (1.0 - b) ** np.clip(r - s, 0, None), 0.0)
+    f = (1.0 - b) ** (np.arange(n) + 1.0)
+    return W, f
+
+
+def abg_matrix(n, alpha, beta, gam):
+    """o = H @ y for the alpha-beta-gamma filter started at x_0 = (y_0, 0, 0):
+    x_i = A x_{i-1} + K y_i with A = (I - K C) F, o_i = C x_i (state-space form)."""
+    F = np.array([[1.0, 1.0, 0.5], [0.0, 1.0, 1.0], [0.0, 0.0, 1.0]])
+    K = np.array([[alpha], [beta], [gam]])
+    C = np.array([[1.0, 0.0, 0.0]])
+    A = (np.eye(3) - K @ C) @ F
+    H = np.zeros((n, n))
+    x0 = np.array([[1.0], [0.0], [0.0]])  # contribution of y_0 through the initial state
+    Ap = np.eye(3)
+    for i in range(n):
+        H[i, 0] = (C @ Ap @ x0)[0, 0]
+        Ap = A @ Ap
+    for j in range(1, n):
+        Ap = np.eye(3)
+        for i in range(j, n):
+            H[i, j] += (C @ Ap @ K)[0, 0]
+            Ap = A @ Ap
+    return H
+
+
+def brute_variant(q, k, v, cu, window, n_sink, gamma, mode, params=(0.0, 0.0, 0.0)):
+    """Delta Attention with the correction of step 5 given by mode (0..4), matrix forms."""
+    out, dense_all, sparse_all = brute_parts(q, k, v, cu, window, n_sink, gamma)
+    if mode == 0:
+        return out
+    res = dense_all.copy()  # tail rows keep the dense result
+    for b in range(len(cu) - 1):
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        L = s1 - s0
+        Lc = (L // gamma) * gamma
+        nA = Lc // gamma
+        if nA == 0:
+            continue
+        for h in range(q.shape[1]):
+            sp = sparse_all[s0:s1, h]
+            dl = delta_rows(dense_all[s0:s1, h], sp, L, gamma)  # [nA, d]
+            if mode == 1:  # recompute: dense rows swapped in at anchors only
+                corr = np.zeros((Lc, sp.shape[1]))
+                corr[::gamma] = dl
+            elif mode == 2:  # linear interpolation towards the next anchor's Delta
+                beta = np.linspace(0.0, 1.0, gamma) if gamma > 1 else np.zeros(1)
+                nxt = np.vstack([dl[1:], dl[-1:]])
+                corr = ((1.0 - beta)[None, :, None] * dl[:, None, :]
+                        + beta[None, :, None] * nxt[:, None, :]).reshape(Lc, -1)
+            elif mode == 3:  # EMA over repeat(Delta, gamma)
+                D = np.repeat(dl, gamma, axis=0)
+                W, f = ema_matrix(Lc, params[0])
+                corr = W @ D + f[:, None] * D[0][None, :]
+            else:  # alpha-beta-gamma filter over Delta_0..Delta_{nA-1}, then repeat
+                H = abg_matrix(nA, *params[:3])
+                corr = np.repeat(H @ dl, gamma, axis=0)
+            res[s0:s0 + Lc, h] = sp[:Lc] + corr
+    return res

@@ -306,3 +306,106 @@ def test_planted_mistake_fails_a_pin(name, tmp_path):
     mutated.write_text(text.replace(old, new))
     lib = oracle.build(force=True, src=str(mutated), dst=str(tmp_path / "libmutant.so"))
     assert not _pins_pass(oracle.Oracle(lib)), f"mutant {name} passed the pins"
+
+
+# ---- correction variants (recompute, interpolation, EMA, alpha-beta-gamma filter) ----
+
+from brute import abg_matrix, brute_variant  # noqa: E402
+
+VARIANT_CASES = [
+    ((300,), 2, 1, 16, 20, 3, 16),
+    ((257,), 4, 2, 16, 9, 0, 7),           # ragged tail, no sinks
+    ((90, 1, 45), 2, 2, 16, 6, 2, 8),      # varlen with a 1-token sequence
+    ((64,), 1, 1, 16, 3, 1, 1),            # gamma 1
+]
+VARIANT_MODES = [(1, (0.0, 0.0, 0.0)), (2, (0.0, 0.0, 0.0)), (3, (0.5, 0.0, 0.0)),
+                 (3, (0.95, 0.0, 0.0)), (4, (0.2, 5e-2, 3.5e-3)), (4, (0.05, 1.25e-4, 2.08e-5))]
+
+
+@pytest.mark.parametrize("case", VARIANT_CASES, ids=[f"v{i}" for i in range(len(VARIANT_CASES))])
+@pytest.mark.parametrize("mode,params", VARIANT_MODES, ids=[f"m{m}-{p[0]}" for m, p in VARIANT_MODES])
+def test_variant_matches_matrix_form(case, mode, params):
+    seqlens, Hq, Hkv, d, w, s, gamma = case
+    (q, k, v), _, cu = rand_problem(seqlens, Hq, Hkv, d, seed=sum(seqlens) + mode)
+    got = oracle.delta_attention_variant(q, k, v, cu, window=w, n_sink=s, gamma=gamma,
+                                         mode=mode, params=params)
+    ref = brute_variant(q, k, v, cu, w, s, gamma, mode, params)
+    np.testing.assert_allclose(got, ref, rtol=0, atol=1e-11)
+
+
+def test_first_anchor_is_always_covered():
+    """Anchor 0 sees only key 0 under both f and f*, so Delta_0 is exactly 0."""
+    (q, k, v), _, cu = rand_problem((50,), 1, 1, 16, seed=22)
+    out, sp, dl = oracle.delta_attention(q, k, v, cu, window=1, n_sink=0, gamma=10,
+                                         return_parts=True)
+    assert np.all(dl[:10] == 0.0)
+
+
+def test_variant_special_cases():
+    (q, k, v), _, cu = rand_problem((400,), 2, 1, 16, seed=21)
+    w, s, g = 30, 2, 16
+    base = oracle.delta_attention(q, k, v, cu, window=w, n_sink=s, gamma=g)
+    var = lambda m, p=(0.0, 0.0, 0.0): oracle.delta_attention_variant(
+        q, k, v, cu, window=w, n_sink=s, gamma=g, mode=m, params=p)
+    dense = oracle.attention(q, k, v, cu, mode=oracle.MODE_DENSE)
+    sparse = oracle.attention(q, k, v, cu, mode=oracle.MODE_SPARSE, window=w, n_sink=s)
+    assert np.array_equal(var(0), base)
+    # EMA with weight 1 keeps the newest value: plain Delta
+    assert np.array_equal(var(3, (1.0, 0, 0)), base)
+    # EMA with weight 0 never moves from D_0 = Delta_0, which is 0 (anchor 0 is covered)
+    np.testing.assert_allclose(var(3, (0.0, 0, 0)), sparse, rtol=0, atol=0)
+    # filter with alpha=1, beta=gamma=0 follows the measurement: plain Delta
+    np.testing.assert_allclose(var(4, (1.0, 0, 0)), base, rtol=0, atol=1e-15)
+    # recompute: dense rows at anchors, sparse rows everywhere else
+    rec = var(1)
+    idx = np.arange(400)
+    np.testing.assert_allclose(rec[idx % g == 0], dense[idx % g == 0], rtol=0, atol=1e-12)
+    assert np.array_equal(rec[idx % g != 0], sparse[idx % g != 0])
+    # interpolation: row a_i carries Delta_i, row a_i + gamma - 1 carries Delta_{i+1}
+    itp = var(2)
+    delta = base - sparse
+    for a in range(0, 400 - 2 * g, g):
+        np.testing.assert_allclose(itp[a] - sparse[a], delta[a], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(itp[a + g - 1] - sparse[a + g - 1], delta[a + g], rtol=0,
+                                   atol=1e-12)
+
+
+def test_abg_matrix_reproduces_constant_and_ramp_tracking():
+    """Independent check of the state-space form: a constant input passes unchanged and
+    a critically-tracked ramp converges (the filter is unbiased for polynomial inputs)."""
+    H = abg_matrix(400, 0.2, 5e-2, 3.5e-3)
+    assert np.allclose(H @ np.ones(400), 1.0, atol=1e-12)
+    ramp = np.arange(400.0)
+    assert abs((H @ ramp)[-1] - ramp[-1]) < 1e-6
+
+
+VARIANT_MUTANTS = {
+    "interp_beta_over_gamma": ("(double)kk / (double)(gamma - 1)", "(double)kk / (double)gamma"),
+    # (starting the EMA from 0 instead of D_0 is no mistake: anchor 0 only sees key 0,
+    # so Delta_0 = D_0 = 0 exactly and both starts agree)
+    "ema_weights_swapped": ("ema[c] = (1.0 - p0) * ema[c] + p0 * dl[i * d + c];",
+                            "ema[c] = p0 * ema[c] + (1.0 - p0) * dl[i * d + c];"),
+    "abg_half_acc_dropped": ("const double pred = pos[c] + vel[c] + 0.5 * acc[c];",
+                             "const double pred = pos[c] + vel[c];"),
+    "recompute_applied_everywhere": ("corr = (kk == 0) ? dl[i * d + c] : 0.0;",
+                                     "corr = dl[i * d + c];"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(VARIANT_MUTANTS))
+def test_planted_variant_mistake_fails_matrix_form(name, tmp_path):
+    src = os.path.join(os.path.dirname(oracle.__file__), "delta_oracle.c")
+    text = open(src).read()
+    old, new = VARIANT_MUTANTS[name]
+    assert text.count(old) == 1, name
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(text.replace(old, new))
+    orc = oracle.Oracle(oracle.build(force=True, src=str(mutated), dst=str(tmp_path / "m.so")))
+    (q, k, v), _, cu = rand_problem((200,), 2, 1, 16, seed=5)
+    failed = False
+    for mode, params in VARIANT_MODES:
+        got = orc.delta_attention_variant(q, k, v, cu, window=12, n_sink=2, gamma=8, mode=mode,
+                                          params=params)
+        ref = brute_variant(q, k, v, cu, 12, 2, 8, mode, params)
+        failed |= not np.allclose(got, ref, rtol=0, atol=1e-11)
+    assert failed, f"mutant {name} passed"
