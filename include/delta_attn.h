@@ -105,6 +105,45 @@ da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, 
                                    unsigned steps);
 
 /*
+ * Correction variants of step 5 of Algorithm 1 (Sec. 3 and the interpolation
+ * appendix): Steps 1-4 as in delta_attn_prefill; then, for the rows r of the
+ * whole groups, out_r = (A*V)_r + c_r with, for anchor a_i = i*gamma and
+ * Delta_i = (A~V)_{a_i} - (A*V)_{a_i}:
+ *   DA_CORR_DELTA      c_r = Delta_{floor(r/gamma)}                    (Eq. 6)
+ *   DA_CORR_RECOMPUTE  c_r = Delta_i at r = a_i, 0 elsewhere: the dense row
+ *                      replaces the sparse one at anchors only         (Eq. 5)
+ *   DA_CORR_INTERP     c_{a_i+k} = (1-b_k) Delta_i + b_k Delta_{i+1},
+ *                      b_k = k/(gamma-1) rising from 0 to 1 over the group;
+ *                      the last group keeps Delta_i.  Uses the next anchor,
+ *                      so it is not causal.
+ *   DA_CORR_EMA        exponential moving average with weight p0 in [0,1]
+ *                      over repeat(Delta, gamma): E_r = (1-p0) E_{r-1} +
+ *                      p0 D_r, E_{-1} = D_0; c_r = E_r
+ *   DA_CORR_ABG        alpha-beta-gamma filter over Delta_0, Delta_1, ...
+ *                      with coefficients (p0, p1, p2) for position, velocity
+ *                      and acceleration; c_r = filtered Delta_{floor(r/gamma)}
+ * Rows past the last whole group take the dense result.  cu_seqlens may be
+ * NULL (B sequences of max_seqlen tokens).  workspace needs
+ * da_workspace_bytes_correction(..., mode) bytes.  Errors as
+ * delta_attn_prefill_varlen, plus DA_ERR_PARAM for an unknown mode, a
+ * non-finite parameter or an EMA weight outside [0,1].
+ */
+#define DA_CORR_DELTA 0
+#define DA_CORR_RECOMPUTE 1
+#define DA_CORR_INTERP 2
+#define DA_CORR_EMA 3
+#define DA_CORR_ABG 4
+da_status delta_attn_prefill_correction(const void* q, const void* k, const void* v, void* out,
+                                        const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                        int Hkv, int d, int window, int n_sink, int gamma,
+                                        int mode, float p0, float p1, float p2, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
+/* Workspace bytes delta_attn_prefill_correction needs (0 if the sizes or mode are invalid). */
+size_t da_workspace_bytes_correction(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma,
+                                     int mode);
+
+/*
  * Sparse attention alone (f*, StreamingLLM sink + window; the first step of
  * Algorithm 1): out_i = (A*V)_i for every row.  Needs no workspace.
  */

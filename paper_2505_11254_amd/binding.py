@@ -21,11 +21,13 @@ LIB_PATH = os.path.join(_HERE, "libdelta_attn.so")
 STATUS = {0: "DA_OK", 1: "DA_ERR_NULL", 2: "DA_ERR_SHAPE", 3: "DA_ERR_PARAM",
           4: "DA_ERR_UNSUPPORTED", 5: "DA_ERR_ALIGN", 6: "DA_ERR_WORKSPACE", 7: "DA_ERR_HIP"}
 
-# C entry points and their argument types: p = pointer, i = int, z = size_t, u = unsigned
+# C entry points and their argument types: p = pointer, i = int, z = size_t, u = unsigned,
+# f = float
 SIGNATURES = {
     "delta_attn_prefill": "ppppiiiiiiiipzp",
     "delta_attn_prefill_varlen": "pppppiiiiiiiipzp",
     "delta_attn_prefill_steps": "pppppiiiiiiiipzpu",
+    "delta_attn_prefill_correction": "pppppiiiiiiiiifffpzp",
     "sparse_attn_prefill": "ppppiiiiiiip",
     "sparse_attn_prefill_varlen": "pppppiiiiiiip",
     "dense_causal_attn_prefill": "ppppiiiiip",
@@ -56,13 +58,15 @@ def load_library(path: str = LIB_PATH):
                            "(hipcc for gfx950); there is no fallback implementation")
     lib = ctypes.CDLL(path)
     codes = {"p": ctypes.c_void_p, "i": ctypes.c_int, "z": ctypes.c_size_t,
-             "u": ctypes.c_uint}
+             "u": ctypes.c_uint, "f": ctypes.c_float}
     for name, sig in SIGNATURES.items():
         f = getattr(lib, name)
         f.argtypes = [codes[c] for c in sig]
         f.restype = ctypes.c_int
     lib.da_workspace_bytes.argtypes = [ctypes.c_int] * 6
     lib.da_workspace_bytes.restype = ctypes.c_size_t
+    lib.da_workspace_bytes_correction.argtypes = [ctypes.c_int] * 7
+    lib.da_workspace_bytes_correction.restype = ctypes.c_size_t
     lib.da_status_string.argtypes = [ctypes.c_int]
     lib.da_status_string.restype = ctypes.c_char_p
     lib.da_last_hip_error.argtypes = []
@@ -133,6 +137,25 @@ def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=Non
 
 
 STEP_SPARSE, STEP_DENSE_ROWS, STEP_CORRECT, STEP_ALL = 1, 2, 4, 7
+CORR_DELTA, CORR_RECOMPUTE, CORR_INTERP, CORR_EMA, CORR_ABG = 0, 1, 2, 3, 4
+
+
+def delta_attn_prefill_correction(q, k, v, *, window, n_sink, gamma, mode,
+                                  params=(0.0, 0.0, 0.0), B=None, cu_seqlens=None,
+                                  max_seqlen=None, out=None, workspace=None, stream=None):
+    """Algorithm 1 with the step-5 correction chosen by ``mode`` (CORR_*)."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    nbytes = int(load_library().da_workspace_bytes_correction(B_, N, Hq, Hkv, d, gamma, mode))
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    wsz = workspace.numel() * workspace.element_size()
+    p = list(params) + [0.0] * (3 - len(params))
+    _call("delta_attn_prefill_correction", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+          _ptr(cu_seqlens), B_, N, Hq, Hkv, d, window, n_sink, gamma, mode, float(p[0]),
+          float(p[1]), float(p[2]), _ptr(workspace), wsz, _stream(q.device, stream))
+    return out
 
 
 def delta_attn_prefill_steps(q, k, v, out, workspace, steps, *, window, n_sink, gamma, B=None,

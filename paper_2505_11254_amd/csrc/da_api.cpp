@@ -3,6 +3,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <cmath>
+
 #include <atomic>
 
 #include "delta_attn.h"
@@ -84,6 +86,12 @@ bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p
   return true;
 }
 
+size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mode) {
+  if (mode < 2 || gamma < 1) return 0;
+  const size_t per = (size_t)B * Hq * (size_t)(max_seqlen / gamma) * d;
+  return mode == 3 ? 2 * per : per;
+}
+
 namespace {
 
 struct Problem {
@@ -150,13 +158,18 @@ da_status run_plain(const Problem& P, bool sparse, void* stream) {
 }
 
 da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, void* stream,
-                    unsigned steps) {
+                    unsigned steps, int corr_mode = 0, float p0 = 0.f, float p1 = 0.f,
+                    float p2 = 0.f) {
   da_status st = validate(P, true, true);
   if (st != DA_OK) return st;
   if (steps < 1u || steps > DA_STEP_ALL) return DA_ERR_PARAM;
+  if (corr_mode < DA_CORR_DELTA || corr_mode > DA_CORR_ABG) return DA_ERR_PARAM;
+  if (!std::isfinite(p0) || !std::isfinite(p1) || !std::isfinite(p2)) return DA_ERR_PARAM;
+  if (corr_mode == DA_CORR_EMA && (p0 < 0.f || p0 > 1.f)) return DA_ERR_PARAM;
   Plan plan;
   if (!make_plan(P.B, P.N, P.Hq, P.Hkv, P.d, P.gamma, &plan)) return DA_ERR_SHAPE;
-  if (!workspace || workspace_bytes < plan.bytes) return DA_ERR_WORKSPACE;
+  const size_t extra = correction_floats(P.B, P.N, P.Hq, P.d, P.gamma, corr_mode) * 4;
+  if (!workspace || workspace_bytes < plan.bytes + extra) return DA_ERR_WORKSPACE;
   if (!aligned16(workspace)) return DA_ERR_ALIGN;
   {
     const int hpw = heads_per_block(P.Hq / P.Hkv);
@@ -179,6 +192,14 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   a.nR_max = plan.nR_max;
   a.nC = plan.nC;
   a.chunk = plan.chunk;
+  a.corr_mode = corr_mode;
+  a.corr_p[0] = p0;
+  a.corr_p[1] = p1;
+  a.corr_p[2] = p2;
+  if (corr_mode >= DA_CORR_INTERP) {
+    a.dbuf = (float*)(ws + plan.bytes);
+    a.ebuf = a.dbuf + (size_t)P.B * P.Hq * (size_t)plan.nA_max * P.d;
+  }
   hipStream_t s = (hipStream_t)stream;
 
   hipError_t e = hipSuccess;
@@ -194,9 +215,11 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
     e = launch_dense_rows(ar, s);
     if (e != hipSuccess) return fail_hip(e);
   }
-  // Steps 4-5: merge, Delta, broadcast-add in place.
+  // Steps 4-5: merge, Delta, broadcast-add in place (or the chosen variant).
   if (steps & DA_STEP_CORRECT) {
     e = launch_delta_epilogue(a, s);
+    if (e != hipSuccess) return fail_hip(e);
+    e = launch_correction(a, s);
     if (e != hipSuccess) return fail_hip(e);
   }
   return DA_OK;
@@ -232,6 +255,23 @@ da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, 
                                    unsigned steps) {
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
   return da::run_delta(P, workspace, workspace_bytes, stream, steps);
+}
+
+da_status delta_attn_prefill_correction(const void* q, const void* k, const void* v, void* out,
+                                        const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                        int Hkv, int d, int window, int n_sink, int gamma,
+                                        int mode, float p0, float p1, float p2, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
+  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, mode, p0, p1, p2);
+}
+
+size_t da_workspace_bytes_correction(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma,
+                                     int mode) {
+  da::Plan p;
+  if (mode < DA_CORR_DELTA || mode > DA_CORR_ABG) return 0;
+  if (!da::make_plan(B, max_seqlen, Hq, Hkv, d, gamma, &p)) return 0;
+  return p.bytes + da::correction_floats(B, max_seqlen, Hq, d, gamma, mode) * 4;
 }
 
 da_status sparse_attn_prefill(const void* q, const void* k, const void* v, void* out, int B,

@@ -48,6 +48,12 @@ struct Args {
   int nC;             // key chunks per dense row (split of the key axis)
   int chunk;          // keys per chunk, a multiple of kKeyTile
   int head_chunk;     // query heads per epilogue workgroup
+
+  // Correction variants of step 5 (see delta_attn_prefill_correction).
+  int corr_mode;      // DA_CORR_*
+  float corr_p[3];    // EMA weight / filter coefficients
+  float* dbuf;        // [B][Hq][nA_max][d]  Delta_i (filtered in place by the filter mode)
+  float* ebuf;        // [B][Hq][nA_max][d]  EMA value entering group i
 };
 
 // Sizes of the Delta path's workspace for a problem; all in elements/bytes.
@@ -58,6 +64,8 @@ struct Plan {
 };
 
 bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p);
+// Extra workspace floats the correction variants need beyond the plan.
+size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mode);
 int heads_per_block(int G);
 
 // Kernel launchers (da_kernels.hip).  Each returns the hipError_t of the launch.
@@ -65,5 +73,6 @@ hipError_t launch_sparse(const Args& a, hipStream_t s);
 hipError_t launch_dense(const Args& a, hipStream_t s);
 hipError_t launch_dense_rows(const Args& a, hipStream_t s);
 hipError_t launch_delta_epilogue(const Args& a, hipStream_t s);
+hipError_t launch_correction(const Args& a, hipStream_t s);
 
 }  // namespace da

@@ -456,7 +456,12 @@ void attn_kernel(Args a) {
 //   tail row:                out[row] = dense.
 // An anchor with a < n_sink + window sees all keys 0..a in its sparse set, so
 // its Delta is exactly zero and the block leaves its rows untouched.
-template <int D>
+// Epilogue modes: the Delta correction itself; "recompute" (Eq. 5: the dense
+// row replaces the sparse one at anchors only); or merge only (Delta_i into
+// dbuf for the other correction variants, tail rows into out).
+enum Epi { kEpiDelta = 0, kEpiRecompute = 1, kEpiMergeOnly = 2 };
+
+template <int D, int EPI>
 __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
   __shared__ float delta[8192];  // [head in range][D]
   const int tid = threadIdx.x;
@@ -475,13 +480,21 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
   if (r >= nR) return;
   const bool anchor = r < nA;
   const int pos = anchor ? r * a.gamma : Lc + (r - nA);
-  if (anchor && (int64_t)pos < (int64_t)a.n_sink + a.window) return;
-
+  const bool covered = anchor && (int64_t)pos < (int64_t)a.n_sink + a.window;
   const int h0 = hc * a.head_chunk;
   const int h1 = min(a.Hq, h0 + a.head_chunk);
   const int nh = h1 - h0;
-  const int nc = (int)(((int64_t)pos + a.chunk) / a.chunk);  // chunks holding keys 0..pos
   constexpr int DC = D / 8;
+  if (covered) {
+    if (EPI == kEpiMergeOnly) {  // Delta_i is exactly zero
+      for (int idx = tid; idx < nh * DC; idx += kEpiThreads) {
+        const int h = h0 + idx / DC, dc = idx % DC;
+        *(f32x8*)(a.dbuf + (((int64_t)b * a.Hq + h) * a.nA_max + r) * D + dc * 8) = f32x8{};
+      }
+    }
+    return;
+  }
+  const int nc = (int)(((int64_t)pos + a.chunk) / a.chunk);  // chunks holding keys 0..pos
   typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
   for (int idx = tid; idx < nh * DC; idx += kEpiThreads) {
@@ -502,13 +515,17 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
     }
     const f32x8 dense = acc * (1.f / lsum);
     uint16_t* orow = a.out + ((sq.base + pos) * a.Hq + h) * (int64_t)D + dc * 8;
-    *(bf16x8_t*)orow = __builtin_convertvector(dense, bf16x8_t);
-    if (anchor) {
-      const f32x8 sp = *(const f32x8*)(a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + r) * D + dc * 8);
-      *(f32x8*)(delta + hh * D + dc * 8) = dense - sp;
+    if (EPI != kEpiMergeOnly || !anchor) *(bf16x8_t*)orow = __builtin_convertvector(dense, bf16x8_t);
+    if (anchor && EPI != kEpiRecompute) {
+      const int64_t arow = (((int64_t)b * a.Hq + h) * a.nA_max + r) * D + dc * 8;
+      const f32x8 dl = dense - *(const f32x8*)(a.sa + arow);
+      if (EPI == kEpiDelta)
+        *(f32x8*)(delta + hh * D + dc * 8) = dl;
+      else
+        *(f32x8*)(a.dbuf + arow) = dl;
     }
   }
-  if (!anchor) return;
+  if (!anchor || EPI != kEpiDelta) return;
   __syncthreads();
 
   // rows pos+1 .. pos+gamma-1 for heads [h0, h1): nh*D contiguous values per row
@@ -522,6 +539,107 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
     const bf16x8_t x = *(const bf16x8_t*)p;
     const f32x8 y = __builtin_convertvector(x, f32x8) + *(const f32x8*)(delta + hh * D + dc * 8);
     *(bf16x8_t*)p = __builtin_convertvector(y, bf16x8_t);
+  }
+}
+
+// Recurrences of the smoothing variants over the anchors of one sequence,
+// one thread per (sequence, head, channel), in anchor order (a group's state
+// needs the previous group's):
+//   EMA (weight w): E_r = (1-w) E_{r-1} + w D_r over D = repeat(Delta, gamma),
+//     E_{-1} = D_0.  Inside group i, D is constant, so with q = 1-w the value
+//     entering the group, Ein_i, gives E_{a_i+k} = q^(k+1) Ein_i +
+//     (1 - q^(k+1)) Delta_i; the scan stores Ein_i and steps
+//     Ein_{i+1} = q^gamma Ein_i + (1 - q^gamma) Delta_i.
+//   alpha-beta-gamma filter (p0, p1, p2): position/velocity/acceleration
+//     update per anchor; Delta_i is replaced by the filtered position.
+template <int CORR>
+__global__ __launch_bounds__(256) void corr_scan_kernel(Args a) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t per_seq = (int64_t)a.Hq * a.d;
+  if (t >= (int64_t)a.B * per_seq) return;
+  const int b = (int)(t / per_seq);
+  const int h = (int)((t % per_seq) / a.d);
+  const int c = (int)(t % a.d);
+  const int nA = seq_of(a, b).L / a.gamma;
+  if (nA == 0) return;
+  float* dl = a.dbuf + ((int64_t)b * a.Hq + h) * a.nA_max * a.d + c;
+  if (CORR == 3) {
+    float* ein = a.ebuf + ((int64_t)b * a.Hq + h) * a.nA_max * a.d + c;
+    const float q = 1.f - a.corr_p[0];
+    const float qg = (q == 0.f) ? 0.f : fast_exp2((float)a.gamma * __log2f(q));
+    float e = dl[0];
+    for (int i = 0; i < nA; ++i) {
+      const float di = dl[(int64_t)i * a.d];
+      ein[(int64_t)i * a.d] = e;
+      e = qg * e + (1.f - qg) * di;
+    }
+  } else {
+    float pos = dl[0], vel = 0.f, acc = 0.f;
+    for (int i = 1; i < nA; ++i) {
+      const float pred = pos + vel + 0.5f * acc;
+      const float vpred = vel + acc;
+      const float res = dl[(int64_t)i * a.d] - pred;
+      pos = pred + a.corr_p[0] * res;
+      vel = vpred + a.corr_p[1] * res;
+      acc = acc + a.corr_p[2] * res;
+      dl[(int64_t)i * a.d] = pos;
+    }
+  }
+}
+
+// Adds the per-row correction of a smoothing variant to the gamma rows of one
+// group, for a range of heads (rows a_i .. a_i+gamma-1, Hq*d contiguous values
+// each):  interpolation (1-beta_k) Delta_i + beta_k Delta_{i+1} with
+// beta_k = k/(gamma-1) (Delta_{i+1} = Delta_i for the last group); EMA
+// q^(k+1) Ein_i + (1 - q^(k+1)) Delta_i; filter: the filtered Delta_i.
+template <int D, int CORR>
+__global__ __launch_bounds__(kEpiThreads) void corr_apply_kernel(Args a) {
+  __shared__ float c0[8192];
+  __shared__ float c1[8192];
+  const int tid = threadIdx.x;
+  int64_t lid = blockIdx.x;
+  const int n_hc = (a.Hq + a.head_chunk - 1) / a.head_chunk;
+  const int hc = (int)(lid % n_hc);
+  lid /= n_hc;
+  const int i = (int)(lid % a.nA_max);
+  const int b = (int)(lid / a.nA_max);
+  const Seq sq = seq_of(a, b);
+  const int nA = sq.L / a.gamma;
+  if (i >= nA) return;
+  const int h0 = hc * a.head_chunk;
+  const int nh = min(a.Hq, h0 + a.head_chunk) - h0;
+  constexpr int DC = D / 8;
+  for (int idx = tid; idx < nh * DC; idx += kEpiThreads) {
+    const int hh = idx / DC, dc = idx % DC;
+    const int64_t row = (((int64_t)b * a.Hq + h0 + hh) * a.nA_max + i) * D + dc * 8;
+    *(f32x8*)(c0 + hh * D + dc * 8) = *(const f32x8*)(a.dbuf + row);
+    if (CORR == 2)
+      *(f32x8*)(c1 + hh * D + dc * 8) = *(const f32x8*)(a.dbuf + row + (i + 1 < nA ? D : 0));
+    if (CORR == 3) *(f32x8*)(c1 + hh * D + dc * 8) = *(const f32x8*)(a.ebuf + row);
+  }
+  __syncthreads();
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+  const int per_row = nh * DC;
+  const int64_t total = (int64_t)a.gamma * per_row;
+  const float lq = (CORR == 3) ? ((a.corr_p[0] >= 1.f) ? -INFINITY : __log2f(1.f - a.corr_p[0])) : 0.f;
+  for (int64_t u = tid; u < total; u += kEpiThreads) {
+    const int kk = (int)(u / per_row);
+    const int rem = (int)(u % per_row);
+    const int hh = rem / DC, dc = rem % DC;
+    const f32x8 di = *(const f32x8*)(c0 + hh * D + dc * 8);
+    f32x8 corr;
+    if (CORR == 2) {
+      const float beta = a.gamma > 1 ? (float)kk / (float)(a.gamma - 1) : 0.f;
+      corr = (1.f - beta) * di + beta * *(const f32x8*)(c1 + hh * D + dc * 8);
+    } else if (CORR == 3) {
+      const float w = fast_exp2((float)(kk + 1) * lq);  // q^(k+1)
+      corr = w * *(const f32x8*)(c1 + hh * D + dc * 8) + (1.f - w) * di;
+    } else {
+      corr = di;
+    }
+    uint16_t* p = a.out + ((sq.base + (int64_t)i * a.gamma + kk) * a.Hq + h0 + hh) * (int64_t)D + dc * 8;
+    const bf16x8_t x = *(const bf16x8_t*)p;
+    *(bf16x8_t*)p = __builtin_convertvector(__builtin_convertvector(x, f32x8) + corr, bf16x8_t);
   }
 }
 
@@ -553,10 +671,51 @@ hipError_t launch_delta_epilogue(const Args& a, hipStream_t s) {
   const int n_hc = (a.Hq + a.head_chunk - 1) / a.head_chunk;
   const int64_t nblocks = (int64_t)a.B * a.nR_max * n_hc;
   if (nblocks <= 0) return hipSuccess;
-  if (a.d == 128)
-    hipLaunchKernelGGL(delta_epilogue_kernel<128>, dim3((unsigned)nblocks), dim3(kEpiThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(delta_epilogue_kernel<64>, dim3((unsigned)nblocks), dim3(kEpiThreads), 0, s, a);
+  const dim3 g((unsigned)nblocks), t(kEpiThreads);
+#define DA_EPI(DD, E) hipLaunchKernelGGL((delta_epilogue_kernel<DD, E>), g, t, 0, s, a)
+  const int epi = a.corr_mode == 0 ? kEpiDelta : a.corr_mode == 1 ? kEpiRecompute : kEpiMergeOnly;
+  if (a.d == 128) {
+    if (epi == kEpiDelta) DA_EPI(128, kEpiDelta);
+    else if (epi == kEpiRecompute) DA_EPI(128, kEpiRecompute);
+    else DA_EPI(128, kEpiMergeOnly);
+  } else {
+    if (epi == kEpiDelta) DA_EPI(64, kEpiDelta);
+    else if (epi == kEpiRecompute) DA_EPI(64, kEpiRecompute);
+    else DA_EPI(64, kEpiMergeOnly);
+  }
+#undef DA_EPI
+  return hipGetLastError();
+}
+
+// After the merge-only epilogue: the scan (EMA, filter) and the apply pass of
+// the smoothing variants (modes 2-4).
+hipError_t launch_correction(const Args& a, hipStream_t s) {
+  if (a.corr_mode < 2) return hipSuccess;
+  if (a.corr_mode >= 3) {
+    const int64_t threads = (int64_t)a.B * a.Hq * a.d;
+    const dim3 g((unsigned)((threads + 255) / 256)), t(256);
+    if (a.corr_mode == 3)
+      hipLaunchKernelGGL(corr_scan_kernel<3>, g, t, 0, s, a);
+    else
+      hipLaunchKernelGGL(corr_scan_kernel<4>, g, t, 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int n_hc = (a.Hq + a.head_chunk - 1) / a.head_chunk;
+  const int64_t nblocks = (int64_t)a.B * a.nA_max * n_hc;
+  if (nblocks <= 0) return hipSuccess;
+  const dim3 g((unsigned)nblocks), t(kEpiThreads);
+#define DA_APPLY(DD, C) hipLaunchKernelGGL((corr_apply_kernel<DD, C>), g, t, 0, s, a)
+  if (a.d == 128) {
+    if (a.corr_mode == 2) DA_APPLY(128, 2);
+    else if (a.corr_mode == 3) DA_APPLY(128, 3);
+    else DA_APPLY(128, 4);
+  } else {
+    if (a.corr_mode == 2) DA_APPLY(64, 2);
+    else if (a.corr_mode == 3) DA_APPLY(64, 3);
+    else DA_APPLY(64, 4);
+  }
+#undef DA_APPLY
   return hipGetLastError();
 }
 

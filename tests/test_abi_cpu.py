@@ -129,3 +129,24 @@ def test_oracle_and_library_share_nothing():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
                 assert "delta_oracle" not in text, f
+
+
+def test_correction_call_rejects_bad_arguments(lib):
+    import ctypes as C
+    f = lib.delta_attn_prefill_correction
+
+    def call(mode, p0=0.0, p1=0.0, p2=0.0, wsz=1 << 40, gamma=16):
+        return f(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 8, 2, 128, 64, 4, gamma, mode,
+                 C.c_float(p0), C.c_float(p1), C.c_float(p2), FAKE, wsz, None)
+    assert call(5) == 3 and call(-1) == 3
+    assert call(3, p0=1.5) == 3 and call(3, p0=-0.1) == 3
+    assert call(4, p1=float("nan")) == 3 and call(4, p2=float("inf")) == 3
+    assert call(2, wsz=16) == 6
+    assert call(3, gamma=0) == 3
+    ws = lib.da_workspace_bytes_correction
+    assert ws(1, 1024, 8, 2, 128, 16, 9) == 0
+    base = lib.da_workspace_bytes(1, 1024, 8, 2, 128, 16)
+    assert ws(1, 1024, 8, 2, 128, 16, 0) == base == ws(1, 1024, 8, 2, 128, 16, 1)
+    per = 8 * (1024 // 16) * 128 * 4
+    assert ws(1, 1024, 8, 2, 128, 16, 2) == base + per == ws(1, 1024, 8, 2, 128, 16, 4)
+    assert ws(1, 1024, 8, 2, 128, 16, 3) == base + 2 * per
