@@ -196,6 +196,40 @@ def gamma_sweep(args, wl, binding, q, k, v, kw, dev):
         del ws
 
 
+CORRECTIONS = [("delta", 0, (0.0, 0.0, 0.0)), ("recompute", 1, (0.0, 0.0, 0.0)),
+               ("linear_interpolation", 2, (0.0, 0.0, 0.0)), ("ema_0.5", 3, (0.5, 0.0, 0.0)),
+               ("abg_filter_0.2", 4, (0.2, 5e-2, 3.5e-3))]
+
+
+def correction_sweep(args, wl, binding, q, k, v, kw, dev):
+    """Time the Delta path with each correction variant of step 5 (same inputs)."""
+    import torch
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(dev)
+    for name, mode, params in CORRECTIONS:
+        nbytes = binding.load_library().da_workspace_bytes_correction(
+            wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma, mode)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        run = lambda: binding.delta_attn_prefill_correction(
+            q, k, v, window=wl.window, n_sink=wl.n_sink, gamma=wl.gamma, mode=mode,
+            params=params, out=out, workspace=ws, **kw)
+        for _ in range(args.warmup):
+            run()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        print(json.dumps({"workload": wl.name, "correction": name, "mode": mode,
+                          "params": list(params), "ms": round(ms, 4),
+                          "tokens_per_s": round(wl.total_tokens / ms * 1e3, 1)}), flush=True)
+        del ws
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,6 +242,9 @@ def main():
     ap.add_argument("--gamma-sweep", default=None,
                     help="comma-separated gammas: time the Delta path and the sparse-only "
                          "kernel at each (one JSON line per gamma) instead of the main record")
+    ap.add_argument("--correction-sweep", action="store_true",
+                    help="time every step-5 correction variant (one JSON line each) instead "
+                         "of the main record")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB device buffer, a dispatch of known traffic "
                          "against which HBM byte counters are scaled")
@@ -243,6 +280,9 @@ def main():
     kw = dict(B=wl.B) if wl.fixed_length else dict(cu_seqlens=cu, max_seqlen=wl.max_seqlen)
     if args.gamma_sweep:
         gamma_sweep(args, wl, binding, q, k, v, kw, dev)
+        return
+    if args.correction_sweep:
+        correction_sweep(args, wl, binding, q, k, v, kw, dev)
         return
     out = torch.empty_like(q)
     ws_bytes = binding.workspace_bytes(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma)

@@ -563,26 +563,43 @@ __global__ __launch_bounds__(256) void corr_scan_kernel(Args a) {
   const int nA = seq_of(a, b).L / a.gamma;
   if (nA == 0) return;
   float* dl = a.dbuf + ((int64_t)b * a.Hq + h) * a.nA_max * a.d + c;
+  // anchors are visited in batches of kB whose loads are all issued before the
+  // recurrence consumes them, so the scan is not bound by one load at a time
+  constexpr int kB = 16;
+  float buf[kB];
   if (CORR == 3) {
     float* ein = a.ebuf + ((int64_t)b * a.Hq + h) * a.nA_max * a.d + c;
     const float q = 1.f - a.corr_p[0];
     const float qg = (q == 0.f) ? 0.f : fast_exp2((float)a.gamma * __log2f(q));
     float e = dl[0];
-    for (int i = 0; i < nA; ++i) {
-      const float di = dl[(int64_t)i * a.d];
-      ein[(int64_t)i * a.d] = e;
-      e = qg * e + (1.f - qg) * di;
+    for (int i0 = 0; i0 < nA; i0 += kB) {
+#pragma unroll
+      for (int j = 0; j < kB; ++j) buf[j] = (i0 + j < nA) ? dl[(int64_t)(i0 + j) * a.d] : 0.f;
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        if (i0 + j < nA) {
+          ein[(int64_t)(i0 + j) * a.d] = e;
+          e = qg * e + (1.f - qg) * buf[j];
+        }
+      }
     }
   } else {
     float pos = dl[0], vel = 0.f, acc = 0.f;
-    for (int i = 1; i < nA; ++i) {
-      const float pred = pos + vel + 0.5f * acc;
-      const float vpred = vel + acc;
-      const float res = dl[(int64_t)i * a.d] - pred;
-      pos = pred + a.corr_p[0] * res;
-      vel = vpred + a.corr_p[1] * res;
-      acc = acc + a.corr_p[2] * res;
-      dl[(int64_t)i * a.d] = pos;
+    for (int i0 = 1; i0 < nA; i0 += kB) {
+#pragma unroll
+      for (int j = 0; j < kB; ++j) buf[j] = (i0 + j < nA) ? dl[(int64_t)(i0 + j) * a.d] : 0.f;
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        if (i0 + j < nA) {
+          const float pred = pos + vel + 0.5f * acc;
+          const float vpred = vel + acc;
+          const float res = buf[j] - pred;
+          pos = pred + a.corr_p[0] * res;
+          vel = vpred + a.corr_p[1] * res;
+          acc = acc + a.corr_p[2] * res;
+          dl[(int64_t)(i0 + j) * a.d] = pos;
+        }
+      }
     }
   }
 }
