@@ -67,6 +67,35 @@ def epilogue_bytes(wl):
     return tot
 
 
+def plan_chunk(wl):
+    """Keys per key chunk of the strided dense rows, as the library plans it:
+    ceil(max_seqlen / 2048) chunks, at most 16 (fewer only when the partial
+    results would pass 8 GiB), rounded up to a multiple of 64 keys."""
+    L = wl.max_seqlen
+    nA = L // wl.gamma
+    nR = nA + min(wl.gamma - 1, L)
+    nC = max(1, min(16, -(-L // 2048)))
+    while nC > 1 and wl.B * wl.Hq * nR * (wl.d + 2) * 4 * nC > (8 << 30):
+        nC -= 1
+    return -(-(-(-L // nC)) // 64) * 64
+
+
+def merge_bytes(wl):
+    """Algorithmic HBM bytes of the fused schedule's merge: for every dense row
+    it merges (anchors whose Delta is not zero, and tail rows), read the fp32
+    partial (d values, max, normaliser) of each key chunk the row reaches and
+    write the merged fp32 row."""
+    chunk = plan_chunk(wl)
+    tot = 0
+    first_open = -(-(wl.n_sink + wl.window) // wl.gamma)
+    for L in wl.seqlens:
+        nA = L // wl.gamma
+        rows = [i * wl.gamma for i in range(first_open, nA)] + list(range(nA * wl.gamma, L))
+        for p_ in rows:
+            tot += ((p_ // chunk + 1) * (wl.d + 2) * 4 + wl.d * 4) * wl.Hq
+    return tot
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("da_kernels.hip", "da_api.cpp", "da_internal.hpp"):
@@ -189,6 +218,8 @@ def gamma_sweep(args, wl, binding, q, k, v, kw, dev):
         ms = e0.elapsed_time(e1) / args.steps
         sp, dr, dc = pair_counts(w2.seqlens, w2.window, w2.n_sink, g)
         print(json.dumps({"workload": wl.name, "gamma": g, "delta_ms": round(ms, 4),
+                          "schedule": ("fused" if binding.fused_supported(w2.Hq, w2.Hkv, g)
+                                       else "unfused"),
                           "sparse_only_ms": round(sparse_ms, 4),
                           "delta_overhead_vs_sparse": round(ms / sparse_ms, 4),
                           "tokens_per_s": round(w2.total_tokens / ms * 1e3, 1),
@@ -292,27 +323,35 @@ def main():
                max_seqlen=wl.max_seqlen)
     stream = torch.cuda.current_stream(dev)
 
+    # the schedule delta_attn_prefill takes for these sizes, one kernel per call
+    fused = binding.fused_supported(wl.Hq, wl.Hkv, wl.gamma)
+    if fused:
+        F = binding.STEP_FUSED
+        order = [("strided_dense_rows", binding.STEP_DENSE_ROWS | F),
+                 ("dense_row_merge", binding.STEP_CORRECT | F),
+                 ("sparse_window", binding.STEP_SPARSE | F)]
+    else:
+        order = [("sparse_window", binding.STEP_SPARSE),
+                 ("strided_dense_rows", binding.STEP_DENSE_ROWS),
+                 ("delta_epilogue", binding.STEP_CORRECT)]
+
     def step(evs=None):
-        # the three kernels of one Delta Attention prefill, events between them
+        # the kernels of one Delta Attention prefill, events between them
         # recorded on the stream they are launched on
+        for i, (_, bits) in enumerate(order):
+            if evs is not None:
+                evs[i].record(stream)
+            binding.delta_attn_prefill_steps(q, k, v, out, ws, bits, **pkw)
         if evs is not None:
-            evs[0].record(stream)
-        binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_SPARSE, **pkw)
-        if evs is not None:
-            evs[1].record(stream)
-        binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_DENSE_ROWS, **pkw)
-        if evs is not None:
-            evs[2].record(stream)
-        binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_CORRECT, **pkw)
-        if evs is not None:
-            evs[3].record(stream)
+            evs[len(order)].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(order) + 1)]
+           for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -325,10 +364,28 @@ def main():
     t_wall = time.perf_counter() - t_wall0
     ms_total = start.elapsed_time(end)
     ms_per_step = ms_total / args.steps
-    k_ms = [sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps for i in range(3)]
-    log(f"delta path: {ms_per_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); "
-        f"sparse {k_ms[0]:.3f} ms, strided dense rows {k_ms[1]:.3f} ms, "
-        f"delta epilogue {k_ms[2]:.3f} ms")
+    k_ms = {name: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps
+            for i, (name, _) in enumerate(order)}
+    log(f"delta path ({'fused' if fused else 'unfused'} schedule): {ms_per_step:.3f} ms/step "
+        f"(wall {1e3 * t_wall / args.steps:.3f}); "
+        + ", ".join(f"{n} {t:.3f} ms" for n, t in k_ms.items()))
+
+    # the unfused schedule on the same inputs (sparse kernel, strided rows, then
+    # the in-place Delta pass over the output), for comparison
+    unfused_ms = None
+    if fused:
+        run_u = lambda: binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_ALL, **pkw)
+        run_u()
+        u0 = torch.cuda.Event(enable_timing=True)
+        u1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        u0.record(stream)
+        for _ in range(args.steps):
+            run_u()
+        u1.record(stream)
+        torch.cuda.synchronize()
+        unfused_ms = u0.elapsed_time(u1) / args.steps
+        log(f"unfused schedule: {unfused_ms:.3f} ms/step")
 
     # sparse attention alone (f*, StreamingLLM) on the same inputs: the cost
     # Delta adds on top of the sparse method it corrects
@@ -361,12 +418,16 @@ def main():
         del out_d
 
     per_kernel = {
-        "sparse_window": {"ms": k_ms[0], "useful_tflops": flops["sparse"] / k_ms[0] / 1e9},
-        "strided_dense_rows": {"ms": k_ms[1],
-                               "useful_tflops": flops["dense_rows"] / k_ms[1] / 1e9},
-        "delta_epilogue": {"ms": k_ms[2], "gbs": epilogue_bytes(wl) / k_ms[2] / 1e6,
-                           "hbm_frac": epilogue_bytes(wl) / k_ms[2] / 1e6 / PEAK_HBM_GBS},
+        "sparse_window": {"ms": k_ms["sparse_window"],
+                          "useful_tflops": flops["sparse"] / k_ms["sparse_window"] / 1e9},
+        "strided_dense_rows": {"ms": k_ms["strided_dense_rows"],
+                               "useful_tflops": flops["dense_rows"] / k_ms["strided_dense_rows"]
+                               / 1e9},
     }
+    hbm_kernel, hbm_bytes = (("dense_row_merge", merge_bytes(wl)) if fused
+                             else ("delta_epilogue", epilogue_bytes(wl)))
+    per_kernel[hbm_kernel] = {"ms": k_ms[hbm_kernel], "gbs": hbm_bytes / k_ms[hbm_kernel] / 1e6,
+                              "hbm_frac": hbm_bytes / k_ms[hbm_kernel] / 1e6 / PEAK_HBM_GBS}
     if dense_ms is not None:
         per_kernel["dense_causal"] = {"ms": dense_ms,
                                       "useful_tflops": flops["dense_causal"] / dense_ms / 1e9}
@@ -399,6 +460,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": dict(wl.describe(), parallelism="single_gpu"),
+        "schedule": "fused" if fused else "unfused",
+        "unfused_ms_per_step": round(unfused_ms, 4) if unfused_ms else None,
         "speedup_vs_dense_causal": round(dense_ms / ms_per_step, 2) if dense_ms else None,
         "sparse_only_ms": round(sparse_only_ms, 4),
         "delta_overhead_vs_sparse": round(ms_per_step / sparse_only_ms, 4),

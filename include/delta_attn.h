@@ -63,8 +63,14 @@ typedef enum {
  * Delta Attention prefill (Algorithm 1), fixed-length batch of B sequences
  * of N tokens.  Writes the corrected output to `out`.
  * workspace: device memory of at least da_workspace_bytes(B, N, Hq, Hkv, d,
- * gamma) bytes, used for the strided rows' partial results and the sparse
- * output at anchors; its contents on entry do not matter.
+ * gamma) bytes, used for the strided rows' partial results and fp32 rows at
+ * the anchors; its contents on entry do not matter.
+ * Two launch schedules compute the result (see delta_attn_prefill_steps);
+ * this call takes the fused one whenever da_fused_supported(Hq, Hkv, gamma),
+ * else the unfused one.  The fused schedule rounds a corrected row to bf16
+ * once (bf16(sparse + Delta)); the unfused one rounds the sparse row first
+ * and again after adding Delta.  Anchor rows, covered groups and dense tail
+ * rows are bitwise the same under both.
  */
 da_status delta_attn_prefill(const void* q, const void* k, const void* v, void* out,
                              int B, int Hq, int Hkv, int N, int d,
@@ -79,30 +85,52 @@ da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v,
 
 /*
  * The steps of Algorithm 1 one at a time, for measuring each kernel on its
- * own.  `steps` is a non-empty subset of the bits below; the steps it names
- * run in this order, on `stream`, with the same buffers:
+ * own.  `steps` is a non-empty subset of DA_STEP_SPARSE, DA_STEP_DENSE_ROWS
+ * and DA_STEP_CORRECT, optionally with DA_STEP_FUSED; the steps it names run
+ * in the schedule's order, on `stream`, with the same buffers.  A later step
+ * reads what earlier calls left in `out` and the workspace.
+ * Unfused schedule (no DA_STEP_FUSED), in this order:
  *   DA_STEP_SPARSE      step 1: A*V for every row into `out`, plus an fp32 copy
  *                       of the anchor rows in the workspace;
  *   DA_STEP_DENSE_ROWS  steps 2-3: A~V at the anchors (Eq. 4) and at the dense
  *                       tail rows, as key-chunk partial results in the workspace;
  *   DA_STEP_CORRECT     steps 4-5 (Eq. 6): merge the partials, form Delta and
  *                       add it to the gamma rows of each group in `out`.
- * Calls with DA_STEP_SPARSE, then DA_STEP_DENSE_ROWS, then DA_STEP_CORRECT
- * (or one call with DA_STEP_ALL) equal one delta_attn_prefill[_varlen] call.
- * A later step reads what earlier calls left in `out` and the workspace.
+ * Fused schedule (DA_STEP_FUSED), in this order:
+ *   DA_STEP_DENSE_ROWS  as above;
+ *   DA_STEP_CORRECT     merge the partials into fp32 dense rows (workspace);
+ *   DA_STEP_SPARSE      steps 1, 4-5: A*V for every row, stored as
+ *                       bf16(A*V + Delta) (Eq. 6) with Delta formed from the
+ *                       anchor's fp32 sparse row inside the kernel; anchor and
+ *                       tail rows store the dense row.
+ * The fused schedule needs every group of gamma rows inside one head's row
+ * slab of a sparse-kernel workgroup (da_fused_supported); otherwise
+ * DA_STEP_FUSED gives DA_ERR_UNSUPPORTED.  All steps of one schedule, in
+ * order (or one call with DA_STEP_ALL, plus DA_STEP_FUSED for the fused
+ * one), equal one delta_attn_prefill[_varlen] call that takes that schedule.
  * cu_seqlens may be NULL: then B sequences of max_seqlen tokens each.
  * Other arguments and errors as delta_attn_prefill_varlen; a `steps` value
- * outside 1..7 gives DA_ERR_PARAM.
+ * with none of the three step bits, or with other bits, gives DA_ERR_PARAM.
  */
 #define DA_STEP_SPARSE 1u
 #define DA_STEP_DENSE_ROWS 2u
 #define DA_STEP_CORRECT 4u
 #define DA_STEP_ALL 7u
+#define DA_STEP_FUSED 8u
 da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, void* out,
                                    const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
                                    int Hkv, int d, int window, int n_sink, int gamma,
                                    void* workspace, size_t workspace_bytes, void* stream,
                                    unsigned steps);
+
+/*
+ * 1 if the fused schedule serves these sizes, else 0: some power of two h
+ * dividing Hq/Hkv, h <= 8, has 256/h (the rows per query head of one sparse
+ * workgroup) a multiple of gamma.  The fused schedule swaps the in-place
+ * correction pass over `out` for a merge of the dense rows before the
+ * sparse kernel, which then stores the corrected rows itself.
+ */
+int da_fused_supported(int Hq, int Hkv, int gamma);
 
 /*
  * Correction variants of step 5 of Algorithm 1 (Sec. 3 and the interpolation
@@ -122,7 +150,9 @@ da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, 
  *   DA_CORR_ABG        alpha-beta-gamma filter over Delta_0, Delta_1, ...
  *                      with coefficients (p0, p1, p2) for position, velocity
  *                      and acceleration; c_r = filtered Delta_{floor(r/gamma)}
- * Rows past the last whole group take the dense result.  cu_seqlens may be
+ * Rows past the last whole group take the dense result.  DA_CORR_DELTA and
+ * DA_CORR_RECOMPUTE take the fused schedule when da_fused_supported() (as
+ * delta_attn_prefill does), the other modes the unfused one.  cu_seqlens may be
  * NULL (B sequences of max_seqlen tokens).  workspace needs
  * da_workspace_bytes_correction(..., mode) bytes.  Errors as
  * delta_attn_prefill_varlen, plus DA_ERR_PARAM for an unknown mode, a

@@ -67,6 +67,8 @@ def load_library(path: str = LIB_PATH):
     lib.da_workspace_bytes.restype = ctypes.c_size_t
     lib.da_workspace_bytes_correction.argtypes = [ctypes.c_int] * 7
     lib.da_workspace_bytes_correction.restype = ctypes.c_size_t
+    lib.da_fused_supported.argtypes = [ctypes.c_int] * 3
+    lib.da_fused_supported.restype = ctypes.c_int
     lib.da_status_string.argtypes = [ctypes.c_int]
     lib.da_status_string.restype = ctypes.c_char_p
     lib.da_last_hip_error.argtypes = []
@@ -115,6 +117,11 @@ def workspace_bytes(B, max_seqlen, Hq, Hkv, d, gamma) -> int:
     return int(load_library().da_workspace_bytes(B, max_seqlen, Hq, Hkv, d, gamma))
 
 
+def fused_supported(Hq, Hkv, gamma) -> bool:
+    """Whether delta_attn_prefill takes the fused schedule for these sizes."""
+    return bool(load_library().da_fused_supported(Hq, Hkv, gamma))
+
+
 def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=None,
                        max_seqlen=None, out=None, workspace=None, stream=None):
     """Delta Attention prefill (Algorithm 1); returns ``out`` [T, Hq, d] bf16."""
@@ -136,7 +143,7 @@ def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=Non
     return out
 
 
-STEP_SPARSE, STEP_DENSE_ROWS, STEP_CORRECT, STEP_ALL = 1, 2, 4, 7
+STEP_SPARSE, STEP_DENSE_ROWS, STEP_CORRECT, STEP_ALL, STEP_FUSED = 1, 2, 4, 7, 8
 CORR_DELTA, CORR_RECOMPUTE, CORR_INTERP, CORR_EMA, CORR_ABG = 0, 1, 2, 3, 4
 
 

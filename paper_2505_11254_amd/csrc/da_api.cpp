@@ -53,6 +53,12 @@ int heads_per_block(int G) {
   return h;
 }
 
+int fused_heads_per_block(int G, int gamma) {
+  for (int h = heads_per_block(G); h >= 1; h /= 2)
+    if (G % h == 0 && (kRowsPerWave * (kAttnWaves / h)) % gamma == 0) return h;
+  return 0;
+}
+
 // Workspace of the Delta path.  Dense rows of a sequence of length L are the
 // floor(L/gamma) anchors plus the L mod gamma tail rows.  Their key axis is
 // split into nC chunks of `chunk` keys (at least 2048), up to 16 of them.
@@ -78,7 +84,7 @@ bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p
   p->nR_max = (int)nR_max;
   p->nC = (int)nC;
   p->chunk = (int)chunk;
-  p->sa_floats = (size_t)B * Hq * nA_max * d;
+  p->sa_floats = (size_t)B * Hq * nR_max * d;  // sparse anchor rows, or merged dense rows
   p->part_o_floats = (size_t)B * Hq * nR_max * nC * d;
   p->part_ml_floats = (size_t)B * Hq * nR_max * nC * 2;
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -157,15 +163,27 @@ da_status run_plain(const Problem& P, bool sparse, void* stream) {
   return DA_OK;
 }
 
+// Launch sequence of the Delta path.  Unfused schedule: sparse kernel (plus
+// the fp32 sparse rows at anchors), strided dense rows, then the epilogue
+// that merges them, forms Delta and adds it to `out` in place.  Fused
+// schedule (when every group of gamma rows fits one head slab of a sparse
+// workgroup, and for the Delta and recompute corrections only): strided
+// dense rows, the merge into fp32 dense rows, then the sparse kernel storing
+// the corrected rows.  `steps` without DA_STEP_FUSED picks the unfused
+// schedule; `auto_fuse` lets the whole-path calls take the fused one.
 da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, void* stream,
-                    unsigned steps, int corr_mode = 0, float p0 = 0.f, float p1 = 0.f,
-                    float p2 = 0.f) {
+                    unsigned steps, bool auto_fuse, int corr_mode = 0, float p0 = 0.f,
+                    float p1 = 0.f, float p2 = 0.f) {
   da_status st = validate(P, true, true);
   if (st != DA_OK) return st;
-  if (steps < 1u || steps > DA_STEP_ALL) return DA_ERR_PARAM;
+  if ((steps & DA_STEP_ALL) == 0u || steps > (DA_STEP_ALL | DA_STEP_FUSED)) return DA_ERR_PARAM;
   if (corr_mode < DA_CORR_DELTA || corr_mode > DA_CORR_ABG) return DA_ERR_PARAM;
   if (!std::isfinite(p0) || !std::isfinite(p1) || !std::isfinite(p2)) return DA_ERR_PARAM;
   if (corr_mode == DA_CORR_EMA && (p0 < 0.f || p0 > 1.f)) return DA_ERR_PARAM;
+  const int fhpw = fused_heads_per_block(P.Hq / P.Hkv, P.gamma);
+  const bool can_fuse = fhpw > 0 && corr_mode <= DA_CORR_RECOMPUTE;
+  if ((steps & DA_STEP_FUSED) && !can_fuse) return DA_ERR_UNSUPPORTED;
+  const bool fused = (steps & DA_STEP_FUSED) || (auto_fuse && can_fuse);
   Plan plan;
   if (!make_plan(P.B, P.N, P.Hq, P.Hkv, P.d, P.gamma, &plan)) return DA_ERR_SHAPE;
   const size_t extra = correction_floats(P.B, P.N, P.Hq, P.d, P.gamma, corr_mode) * 4;
@@ -178,6 +196,11 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
     if ((int64_t)P.B * (P.Hq / hpw) * plan.nC * rtiles > INT32_MAX) return DA_ERR_SHAPE;
     if ((int64_t)P.B * plan.nR_max * ((P.Hq + 8192 / P.d - 1) / (8192 / P.d)) > INT32_MAX)
       return DA_ERR_SHAPE;
+    if (fused) {
+      const int64_t frows = (int64_t)kRowsPerWave * (kAttnWaves / fhpw);
+      if ((int64_t)P.B * (P.Hq / fhpw) * ((P.N + frows - 1) / frows) > INT32_MAX)
+        return DA_ERR_SHAPE;
+    }
   }
   st = check_device();
   if (st != DA_OK) return st;
@@ -203,6 +226,30 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   hipStream_t s = (hipStream_t)stream;
 
   hipError_t e = hipSuccess;
+  if (fused) {
+    a.dense = a.sa;
+    a.fuse = corr_mode == DA_CORR_RECOMPUTE ? 2 : 1;
+    if (steps & DA_STEP_DENSE_ROWS) {
+      Args ar = a;
+      ar.n_rtiles = (plan.nR_max + kRowsPerWave * a.ppw - 1) / (kRowsPerWave * a.ppw);
+      e = launch_dense_rows(ar, s);
+      if (e != hipSuccess) return fail_hip(e);
+    }
+    if (steps & DA_STEP_CORRECT) {
+      e = launch_delta_epilogue(a, s);
+      if (e != hipSuccess) return fail_hip(e);
+    }
+    if (steps & DA_STEP_SPARSE) {
+      Args as = a;
+      as.hpw = fhpw;
+      as.ppw = kAttnWaves / fhpw;
+      as.n_hgroups = P.Hq / fhpw;
+      as.n_rtiles = (P.N + kRowsPerWave * as.ppw - 1) / (kRowsPerWave * as.ppw);
+      e = launch_sparse(as, s);
+      if (e != hipSuccess) return fail_hip(e);
+    }
+    return DA_OK;
+  }
   // Step 1: sparse attention for every row (+ fp32 copy at anchors).
   if (steps & DA_STEP_SPARSE) {
     e = launch_sparse(a, s);
@@ -236,7 +283,7 @@ da_status delta_attn_prefill(const void* q, const void* k, const void* v, void* 
                              int Hq, int Hkv, int N, int d, int window, int n_sink, int gamma,
                              void* workspace, size_t workspace_bytes, void* stream) {
   Problem P{q, k, v, out, nullptr, B, N, Hq, Hkv, d, window, n_sink, gamma};
-  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL);
+  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, true);
 }
 
 da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v, void* out,
@@ -245,7 +292,7 @@ da_status delta_attn_prefill_varlen(const void* q, const void* k, const void* v,
                                     void* workspace, size_t workspace_bytes, void* stream) {
   if (!cu_seqlens) return DA_ERR_NULL;
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
-  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL);
+  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, true);
 }
 
 da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, void* out,
@@ -254,7 +301,7 @@ da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, 
                                    void* workspace, size_t workspace_bytes, void* stream,
                                    unsigned steps) {
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
-  return da::run_delta(P, workspace, workspace_bytes, stream, steps);
+  return da::run_delta(P, workspace, workspace_bytes, stream, steps, false);
 }
 
 da_status delta_attn_prefill_correction(const void* q, const void* k, const void* v, void* out,
@@ -263,7 +310,8 @@ da_status delta_attn_prefill_correction(const void* q, const void* k, const void
                                         int mode, float p0, float p1, float p2, void* workspace,
                                         size_t workspace_bytes, void* stream) {
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
-  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, mode, p0, p1, p2);
+  return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, true, mode, p0, p1,
+                       p2);
 }
 
 size_t da_workspace_bytes_correction(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma,
@@ -302,6 +350,11 @@ da_status dense_causal_attn_prefill_varlen(const void* q, const void* k, const v
   if (!cu_seqlens) return DA_ERR_NULL;
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, 1, 0, 1};
   return da::run_plain(P, false, stream);
+}
+
+int da_fused_supported(int Hq, int Hkv, int gamma) {
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || gamma < 1) return 0;
+  return da::fused_heads_per_block(Hq / Hkv, gamma) > 0 ? 1 : 0;
 }
 
 size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma) {

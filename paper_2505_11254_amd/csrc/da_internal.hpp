@@ -41,6 +41,8 @@ struct Args {
 
   // Workspace of the Delta path (nullptr for the plain attention calls).
   float* sa;          // [B][Hq][nA_max][d]      sparse output at anchor rows, fp32
+  float* dense;       // [B][Hq][nR_max][d]      merged dense rows, fp32 (fused schedule;
+                      //                          the same memory as sa)
   float* part_o;      // [B][Hq][nR_max][nC][d]  unnormalised partial outputs of dense rows
   float* part_ml;     // [B][Hq][nR_max][nC][2]  (running max * scale_log2, normaliser)
   int nA_max;         // max anchors per sequence: floor(max_seqlen / gamma)
@@ -54,12 +56,16 @@ struct Args {
   float corr_p[3];    // EMA weight / filter coefficients
   float* dbuf;        // [B][Hq][nA_max][d]  Delta_i (filtered in place by the filter mode)
   float* ebuf;        // [B][Hq][nA_max][d]  EMA value entering group i
+
+  // Fused schedule: the sparse kernel stores the corrected rows itself from the
+  // merged dense rows (0: plain sparse store; 1: Delta correction; 2: recompute).
+  int fuse;
 };
 
 // Sizes of the Delta path's workspace for a problem; all in elements/bytes.
 struct Plan {
   int nA_max, nR_max, nC, chunk;
-  size_t sa_floats, part_o_floats, part_ml_floats;
+  size_t sa_floats, part_o_floats, part_ml_floats;  // sa: nR_max rows per (sequence, head)
   size_t bytes;
 };
 
@@ -67,6 +73,10 @@ bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p
 // Extra workspace floats the correction variants need beyond the plan.
 size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mode);
 int heads_per_block(int G);
+// Heads per workgroup of the fused sparse kernel: the largest power of two
+// dividing G (at most kAttnWaves) whose per-head row slab, 32 * kAttnWaves /
+// hpw rows, is a multiple of gamma; 0 when there is none.
+int fused_heads_per_block(int G, int gamma);
 
 // Kernel launchers (da_kernels.hip).  Each returns the hipError_t of the launch.
 hipError_t launch_sparse(const Args& a, hipStream_t s);

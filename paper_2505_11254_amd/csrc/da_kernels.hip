@@ -7,7 +7,10 @@
 //      (Eq. 6); rows after the last whole group are computed densely
 //      (implementation-details appendix).
 // Steps 1 and 2 and the dense causal baseline share one attention kernel
-// template (`attn_kernel`); step 3 is `delta_epilogue_kernel`.
+// template (`attn_kernel`); step 3 is `delta_epilogue_kernel`.  The fused
+// schedule runs step 2 first, merges its dense rows, and lets the sparse
+// kernel store sparse + Delta directly, which saves the in-place pass over
+// the output.
 //
 // Tile core (one wavefront = 32 query rows, 64-key tiles, bf16 MFMA):
 //   S^T[key][row] = K Q^T   with v_mfma_f32_32x32x16_bf16: A = K rows from
@@ -72,14 +75,28 @@ __device__ __forceinline__ Seq seq_of(const Args& a, int b) {
   return {(int64_t)b * a.N, a.N};
 }
 
-// Workgroups are dispatched round-robin over the 8 XCDs (block i -> XCD i % 8),
-// each with its own L2.  Give XCD x the contiguous logical range
-// [x*n/8, (x+1)*n/8) so neighbouring tiles, which read overlapping key/value
-// ranges, share one L2.
-__device__ __forceinline__ int64_t xcd_remap(int64_t i, int64_t n) {
-  const int64_t per = n / 8;
-  if (i < per * 8) return (i % 8) * per + i / 8;
-  return i;
+// Workgroups are dispatched in order, round-robin over the 8 XCDs (block i ->
+// XCD i % 8), each with its own L2.  Logical blocks are ordered head group
+// outermost, then sequence, [key chunk,] row tile.
+//  - When the head groups split evenly over the XCDs, XCD x takes the
+//    contiguous eighth [x*n/8, (x+1)*n/8): whole head groups, each with every
+//    sequence, so the XCDs get equal work and each streams its own kv heads'
+//    keys and values through its L2 while neighbouring tiles share them.
+//  - Otherwise XCD x takes the logical chunks x, x+8, x+16, ... of kXcdChunk
+//    consecutive blocks: neighbouring tiles still run together on one L2,
+//    and all XCDs walk the logical order at the same pace, which spreads
+//    uneven work (sequences of different lengths, triangular key ranges).
+//    Blocks past the last whole round of 8 chunks keep their index.
+constexpr int kXcdChunk = 64;
+__device__ __forceinline__ int64_t xcd_remap(int64_t i, int64_t n, bool contiguous) {
+  if (contiguous) {
+    const int64_t per = n / 8;
+    return i < per * 8 ? (i % 8) * per + i / 8 : i;
+  }
+  const int64_t span = 8 * (int64_t)kXcdChunk;
+  if (i >= n / span * span) return i;
+  const int64_t k = i / 8;
+  return ((i % 8) + 8 * (k / kXcdChunk)) * kXcdChunk + k % kXcdChunk;
 }
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -122,7 +139,12 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2)
 void attn_kernel(Args a) {
   using LD = Lds<D>;
   constexpr int NS = kAttnStages;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[NS * LD::stageElems];
+  // The sparse kernel also holds, after the K/V ring, the fp32 dense rows of
+  // its block's anchors for the fused store: hpw * (slab rows / gamma) rows
+  // of D floats, at most 128 * D floats (gamma >= 2).
+  constexpr int kPreFloats = (MODE == kSparse) ? 128 * D : 0;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[NS * LD::stageElems + 2 * kPreFloats];
+  float* const dpre = (float*)(smem + NS * LD::stageElems);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -131,7 +153,7 @@ void attn_kernel(Args a) {
   const int col = lane & 31;
 
   // ---- which (sequence, head group, row tile[, key chunk]) this block owns
-  int64_t lid = xcd_remap(blockIdx.x, gridDim.x);
+  int64_t lid = xcd_remap(blockIdx.x, gridDim.x, a.n_hgroups % 8 == 0);
   int rt = (int)(lid % a.n_rtiles);
   lid /= a.n_rtiles;
   int c = 0;
@@ -139,8 +161,8 @@ void attn_kernel(Args a) {
     c = (int)(lid % a.nC);
     lid /= a.nC;
   }
-  const int hg = (int)(lid % a.n_hgroups);
-  const int b = (int)(lid / a.n_hgroups);
+  const int b = (int)(lid % a.B);
+  const int hg = (int)(lid / a.B);
   // Longest rows first: in the dense modes blocks dispatched together then have
   // (nearly) the same number of key tiles, start on the same tile and stay in
   // step, so they share each key/value tile in L2.
@@ -202,6 +224,23 @@ void attn_kernel(Args a) {
     const uint16_t* qp = a.q + ((sq.base + pos_ld) * a.Hq + h) * (int64_t)D + half * 8;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + kk * 16);
+    // Fused store: fetch the merged dense rows of the block's anchors whose
+    // Delta is not zero (anchor slot = head in block * groups per slab +
+    // group in slab), so the epilogue does not wait on memory.
+    if (MODE == kSparse && a.fuse && a.gamma > 1) {
+      const int per_slab = kRowsPerWave * a.ppw / a.gamma;
+      const int a_end = min(R1, Lc);
+      const int nvec = a.hpw * per_slab * (D / 4);
+      for (int u = tid; u < nvec; u += kAttnThreads) {
+        const int slot = u / (D / 4), dv = u % (D / 4);
+        const int apos = R0 + (slot % per_slab) * a.gamma;
+        if (apos < a_end && (int64_t)apos >= (int64_t)a.n_sink + a.window) {
+          const int hh = hg * a.hpw + slot / per_slab;
+          *(f32x4*)(dpre + slot * D + dv * 4) = *(const f32x4*)(
+              a.dense + (((int64_t)b * a.Hq + hh) * a.nR_max + apos / a.gamma) * D + dv * 4);
+        }
+      }
+    }
     // retire the Q loads here (vmcnt(0)): the main loop's MFMAs read qf every
     // iteration and must not wait behind the prefetch loads issued in it
     __builtin_amdgcn_s_waitcnt(0x0F70);
@@ -410,6 +449,63 @@ void attn_kernel(Args a) {
 
   // ---- epilogue: output register r of block mb is dim 32*mb + 8*(r/4) + 4*half + r%4
   const float lt = l + __shfl_xor(l, 32);
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  if (MODE == kSparse && a.fuse) {
+    // Fused Delta store (the dense rows were merged into a.dense beforehand).
+    // Every group of gamma rows lies inside one head's row slab of this block,
+    // so its anchor's sparse row is in a register of some lane here: the
+    // anchor lane forms Delta = dense - sparse in fp32 over the dense row the
+    // prologue staged in LDS and leaves it there for the group's other rows,
+    // which store bf16(sparse + Delta), one rounding.  Anchor rows store the
+    // dense row, tail rows (past the last whole group) the dense row too;
+    // groups whose anchor a < n_sink + window have Delta = 0 exactly and keep
+    // the sparse row untouched.  Recompute (fuse 2) replaces anchors only.
+    const float inv = 1.f / lt;
+    const bool in_c = row_valid && my_pos < Lc;
+    const int anc = in_c ? my_pos - my_pos % a.gamma : 0;
+    const bool open = in_c && (int64_t)anc >= (int64_t)a.n_sink + a.window;
+    const bool is_anchor = open && anc == my_pos;
+    const bool staged = a.gamma > 1;  // anchor dense rows are in dpre
+    const int xslot =
+        ((wave % a.hpw) * (kRowsPerWave * a.ppw / a.gamma) + (in_c ? (my_pos - R0) / a.gamma : 0)) * D;
+    uint16_t* orow = a.out + ((sq.base + (row_valid ? my_pos : 0)) * a.Hq + h) * (int64_t)D;
+    if (a.fuse == 1 && staged) {
+      if (is_anchor) {
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+          for (int jq = 0; jq < 4; ++jq) {
+            const int dim = 32 * mb + 8 * jq + 4 * half;
+            const f32x4 sv = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv,
+                              o[mb][4 * jq + 2] * inv, o[mb][4 * jq + 3] * inv};
+            const f32x4 dv = *(const f32x4*)(dpre + xslot + dim);
+            *(f32x4*)(dpre + xslot + dim) = dv - sv;
+            *(bf16x4*)(orow + dim) = __builtin_convertvector(dv, bf16x4);
+          }
+      }
+      __syncthreads();  // Delta of every group is in dpre
+      if (is_anchor) return;
+    }
+    if (!row_valid) return;
+    const bool tail = my_pos >= Lc;
+    const bool add = a.fuse == 1 && staged && open;
+    const float* gdrow =  // dense row in global memory: tail rows, and anchors when not staged
+        a.dense + (((int64_t)b * a.Hq + h) * a.nR_max + (in_c ? my_pos / a.gamma : nA + (my_pos - Lc))) * D;
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb) {
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int dim = 32 * mb + 8 * jq + 4 * half;
+        f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
+                     o[mb][4 * jq + 3] * inv};
+        if (tail || (is_anchor && !staged)) val = *(const f32x4*)(gdrow + dim);
+        else if (is_anchor) val = *(const f32x4*)(dpre + xslot + dim);
+        else if (add) val += *(const f32x4*)(dpre + xslot + dim);
+        *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
+      }
+    }
+    return;
+  }
   if (!row_valid) return;
   if (MODE != kDenseRows) {
     const float inv = 1.f / lt;
@@ -424,7 +520,6 @@ void attn_kernel(Args a) {
         const int dim = 32 * mb + 8 * jq + 4 * half;
         f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
                      o[mb][4 * jq + 3] * inv};
-        typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
         *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
         if (write_sa) *(f32x4*)(sarow + dim) = val;
       }
@@ -457,9 +552,12 @@ void attn_kernel(Args a) {
 // An anchor with a < n_sink + window sees all keys 0..a in its sparse set, so
 // its Delta is exactly zero and the block leaves its rows untouched.
 // Epilogue modes: the Delta correction itself; "recompute" (Eq. 5: the dense
-// row replaces the sparse one at anchors only); or merge only (Delta_i into
-// dbuf for the other correction variants, tail rows into out).
-enum Epi { kEpiDelta = 0, kEpiRecompute = 1, kEpiMergeOnly = 2 };
+// row replaces the sparse one at anchors only); merge only (Delta_i into
+// dbuf for the other correction variants, tail rows into out); or, for the
+// fused schedule, which runs before the sparse kernel, the merged dense rows
+// into a.dense in fp32 (covered anchors are skipped: their groups keep the
+// sparse rows).
+enum Epi { kEpiDelta = 0, kEpiRecompute = 1, kEpiMergeOnly = 2, kEpiMergeDense = 3 };
 
 template <int D, int EPI>
 __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
@@ -514,6 +612,10 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
       acc += w * po;
     }
     const f32x8 dense = acc * (1.f / lsum);
+    if (EPI == kEpiMergeDense) {
+      *(f32x8*)(a.dense + (((int64_t)b * a.Hq + h) * a.nR_max + r) * D + dc * 8) = dense;
+      continue;
+    }
     uint16_t* orow = a.out + ((sq.base + pos) * a.Hq + h) * (int64_t)D + dc * 8;
     if (EPI != kEpiMergeOnly || !anchor) *(bf16x8_t*)orow = __builtin_convertvector(dense, bf16x8_t);
     if (anchor && EPI != kEpiRecompute) {
@@ -690,15 +792,19 @@ hipError_t launch_delta_epilogue(const Args& a, hipStream_t s) {
   if (nblocks <= 0) return hipSuccess;
   const dim3 g((unsigned)nblocks), t(kEpiThreads);
 #define DA_EPI(DD, E) hipLaunchKernelGGL((delta_epilogue_kernel<DD, E>), g, t, 0, s, a)
-  const int epi = a.corr_mode == 0 ? kEpiDelta : a.corr_mode == 1 ? kEpiRecompute : kEpiMergeOnly;
+  const int epi = a.fuse ? kEpiMergeDense
+                         : a.corr_mode == 0 ? kEpiDelta
+                         : a.corr_mode == 1 ? kEpiRecompute : kEpiMergeOnly;
   if (a.d == 128) {
     if (epi == kEpiDelta) DA_EPI(128, kEpiDelta);
     else if (epi == kEpiRecompute) DA_EPI(128, kEpiRecompute);
-    else DA_EPI(128, kEpiMergeOnly);
+    else if (epi == kEpiMergeOnly) DA_EPI(128, kEpiMergeOnly);
+    else DA_EPI(128, kEpiMergeDense);
   } else {
     if (epi == kEpiDelta) DA_EPI(64, kEpiDelta);
     else if (epi == kEpiRecompute) DA_EPI(64, kEpiRecompute);
-    else DA_EPI(64, kEpiMergeOnly);
+    else if (epi == kEpiMergeOnly) DA_EPI(64, kEpiMergeOnly);
+    else DA_EPI(64, kEpiMergeDense);
   }
 #undef DA_EPI
   return hipGetLastError();
