@@ -276,6 +276,10 @@ def main():
     ap.add_argument("--correction-sweep", action="store_true",
                     help="time every step-5 correction variant (one JSON line each) instead "
                          "of the main record")
+    ap.add_argument("--path-only", action="store_true",
+                    help="time only the Delta path (and the dense baseline unless --no-dense): "
+                         "skip the unfused-schedule and sparse-only comparison runs, so a "
+                         "profiled run holds the path's own launches")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB device buffer, a dispatch of known traffic "
                          "against which HBM byte counters are scaled")
@@ -373,7 +377,7 @@ def main():
     # the unfused schedule on the same inputs (sparse kernel, strided rows, then
     # the in-place Delta pass over the output), for comparison
     unfused_ms = None
-    if fused:
+    if fused and not args.path_only:
         run_u = lambda: binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_ALL, **pkw)
         run_u()
         u0 = torch.cuda.Event(enable_timing=True)
@@ -389,8 +393,11 @@ def main():
 
     # sparse attention alone (f*, StreamingLLM) on the same inputs: the cost
     # Delta adds on top of the sparse method it corrects
-    sparse_only_ms = time_sparse_only(binding, q, k, v, out, kw, wl, stream, args.steps)
-    log(f"sparse only: {sparse_only_ms:.3f} ms; delta overhead x{ms_per_step / sparse_only_ms:.3f}")
+    sparse_only_ms = None
+    if not args.path_only:
+        sparse_only_ms = time_sparse_only(binding, q, k, v, out, kw, wl, stream, args.steps)
+        log(f"sparse only: {sparse_only_ms:.3f} ms; "
+            f"delta overhead x{ms_per_step / sparse_only_ms:.3f}")
 
     T = wl.total_tokens
     sp_pairs, dr_pairs, dc_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
@@ -463,8 +470,9 @@ def main():
         "schedule": "fused" if fused else "unfused",
         "unfused_ms_per_step": round(unfused_ms, 4) if unfused_ms else None,
         "speedup_vs_dense_causal": round(dense_ms / ms_per_step, 2) if dense_ms else None,
-        "sparse_only_ms": round(sparse_only_ms, 4),
-        "delta_overhead_vs_sparse": round(ms_per_step / sparse_only_ms, 4),
+        "sparse_only_ms": round(sparse_only_ms, 4) if sparse_only_ms else None,
+        "delta_overhead_vs_sparse": (round(ms_per_step / sparse_only_ms, 4) if sparse_only_ms
+                                     else None),
         "dense_causal_ms": round(dense_ms, 3) if dense_ms else None,
         "kernels": {n: {kk: round(vv, 4) for kk, vv in d_.items()} for n, d_ in per_kernel.items()},
         "roofline": roofline,
