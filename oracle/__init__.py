@@ -59,8 +59,18 @@ def _bind(path):
     lib.dao_delta_attention_variant.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, i32,
                                                 i32, i32, i32, ctypes.c_double, ctypes.c_double,
                                                 ctypes.c_double, vp, i32]
+    lib.dao_block_attention.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp, vp, i32,
+                                        i32, vp, i64, vp, i32]
+    lib.dao_block_delta_attention.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp, vp,
+                                              i32, i32, i32, vp, vp, vp, i32]
+    lib.dao_block_delta_attention_rows.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp,
+                                                   vp, i32, i32, i32, vp, i64, vp, vp, i32]
+    lib.dao_block_attention_weights.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, i32, vp, vp,
+                                                i32, i32, i32, i32, i64, vp, vp]
     for f in (lib.dao_attention, lib.dao_attention_weights, lib.dao_delta_attention,
-              lib.dao_delta_attention_rows, lib.dao_delta_attention_variant):
+              lib.dao_delta_attention_rows, lib.dao_delta_attention_variant,
+              lib.dao_block_attention, lib.dao_block_delta_attention,
+              lib.dao_block_delta_attention_rows, lib.dao_block_attention_weights):
         f.restype = ctypes.c_int
     lib.dao_max_threads.restype = ctypes.c_int
     lib.dao_max_threads.argtypes = []
@@ -202,6 +212,108 @@ class Oracle:
                                                 nthreads)
         _check(rc, "delta_attention_rows")
         return (out, dl) if return_delta else out
+
+
+class _Blocks:
+    """Key-block lists in CSR form: ``ptr`` [B, Hkv, nqb + 1] offsets into ``idx``
+    (key tile indices, tiles of 64 keys, local to each sequence), query blocks of
+    ``block_q`` rows."""
+
+    def __init__(self, P, ptr, idx, block_q):
+        self.ptr = np.ascontiguousarray(np.asarray(ptr, dtype=np.int64))
+        self.idx = np.ascontiguousarray(np.asarray(idx, dtype=np.int64).reshape(-1))
+        if self.ptr.ndim != 3 or self.ptr.shape[:2] != (P.B, P.Hkv):
+            raise ValueError("block ptr must be [B, Hkv, nqb + 1]")
+        self.nqb = self.ptr.shape[2] - 1
+        self.block_q = int(block_q)
+        if self.idx.size == 0:
+            self.idx = np.zeros(1, dtype=np.int64)
+
+    def args(self):
+        return self.ptr.ctypes.data, self.idx.ctypes.data, self.nqb, self.block_q
+
+
+def _block_attention(self, q, k, v, cu=None, *, blk_ptr, blk_idx, block_q, rows=None,
+                     nthreads=0):
+    """Sparse attention whose key sets come from key-block lists (see
+    ``delta_oracle.c``): ``[T, Hq, d]``, or ``[n_rows, d]`` for (b, h, i) rows."""
+    P = _Problem(q, k, v, cu)
+    Bl = _Blocks(P, blk_ptr, blk_idx, block_q)
+    if rows is None:
+        out = np.zeros((P.T, P.Hq, P.d))
+        rp, nr = None, 0
+    else:
+        r = _rows_array(rows)
+        out = np.zeros((len(r), P.d))
+        rp, nr = r.ctypes.data, len(r)
+    rc = self._lib.dao_block_attention(*P.ptrs(), *Bl.args(), rp, nr, out.ctypes.data, nthreads)
+    _check(rc, "block_attention")
+    return out
+
+
+def _block_delta_attention(self, q, k, v, cu=None, *, blk_ptr, blk_idx, block_q, gamma,
+                           nthreads=0, return_parts=False):
+    """Algorithm 1 with f* from key-block lists: ``[T, Hq, d]`` fp64 (plus the
+    sparse output and the per-row correction with ``return_parts``)."""
+    P = _Problem(q, k, v, cu)
+    Bl = _Blocks(P, blk_ptr, blk_idx, block_q)
+    out = np.zeros((P.T, P.Hq, P.d))
+    sp = np.zeros((P.T, P.Hq, P.d)) if return_parts else None
+    dl = np.zeros((P.T, P.Hq, P.d)) if return_parts else None
+    rc = self._lib.dao_block_delta_attention(*P.ptrs(), *Bl.args(), gamma, out.ctypes.data,
+                                             sp.ctypes.data if sp is not None else None,
+                                             dl.ctypes.data if dl is not None else None,
+                                             nthreads)
+    _check(rc, "block_delta_attention")
+    return (out, sp, dl) if return_parts else out
+
+
+def _block_delta_attention_rows(self, q, k, v, cu=None, *, blk_ptr, blk_idx, block_q, gamma,
+                                rows, nthreads=0):
+    """Algorithm 1 with f* from key-block lists, at selected (b, h, i) rows."""
+    P = _Problem(q, k, v, cu)
+    Bl = _Blocks(P, blk_ptr, blk_idx, block_q)
+    r = _rows_array(rows)
+    out = np.zeros((len(r), P.d))
+    rc = self._lib.dao_block_delta_attention_rows(*P.ptrs(), *Bl.args(), gamma, r.ctypes.data,
+                                                  len(r), out.ctypes.data, None, nthreads)
+    _check(rc, "block_delta_attention_rows")
+    return out
+
+
+def _block_attention_weights(self, q, k, v, cu=None, *, blk_ptr, blk_idx, block_q, b=0, h=0,
+                             i=0):
+    """Softmax weights of row (b, h, i) under key-block lists, and its output."""
+    P = _Problem(q, k, v, cu)
+    Bl = _Blocks(P, blk_ptr, blk_idx, block_q)
+    w = np.zeros(i + 1)
+    o = np.zeros(P.d)
+    rc = self._lib.dao_block_attention_weights(*P.ptrs(), *Bl.args(), b, h, i, w.ctypes.data,
+                                               o.ctypes.data)
+    _check(rc, "block_attention_weights")
+    return w, o
+
+
+Oracle.block_attention = _block_attention
+Oracle.block_delta_attention = _block_delta_attention
+Oracle.block_delta_attention_rows = _block_delta_attention_rows
+Oracle.block_attention_weights = _block_attention_weights
+
+
+def block_attention(*args, **kw):
+    return Oracle().block_attention(*args, **kw)
+
+
+def block_delta_attention(*args, **kw):
+    return Oracle().block_delta_attention(*args, **kw)
+
+
+def block_delta_attention_rows(*args, **kw):
+    return Oracle().block_delta_attention_rows(*args, **kw)
+
+
+def block_attention_weights(*args, **kw):
+    return Oracle().block_attention_weights(*args, **kw)
 
 
 def _variant(self, q, k, v, cu=None, *, window, n_sink, gamma, mode, params=(0.0, 0.0, 0.0),

@@ -42,6 +42,19 @@
  *
  * Layout: token-major contiguous tensors, q/out [T, Hq, d], k/v [T, Hkv, d];
  * sequence b occupies rows [cu[b], cu[b+1]).
+ *
+ * Other sparse bases (the method corrects any sparse attention f*: Sec. 3,
+ * and the MInference/HiP/Star-Attention comparisons of Sec. 4): f* given by
+ * key-block lists.  Keys are grouped in tiles of 64 positions and query rows
+ * in blocks of block_q rows (positions local to the sequence).  For sequence
+ * b, kv head g and query block qb, the list holds the key tiles that the
+ * block's rows attend to; the tiles overlapping the query block itself
+ * (tile >= qb*block_q/64) are always attended; listed entries outside
+ * [0, qb*block_q/64) are ignored.  Row i then sees
+ *   S(i) = { j <= i : tile(j) listed for (b, kv(h), i / block_q) or
+ *                     tile(j) >= (i / block_q) * block_q / 64 },
+ * normalised over S(i) only, and Algorithm 1 runs unchanged on top.
+ * Lists are CSR: ptr [B][Hkv][nqb + 1] offsets into idx.
  */
 #include <math.h>
 #include <stdint.h>
@@ -57,6 +70,8 @@
 
 #define DAO_MODE_DENSE 0
 #define DAO_MODE_SPARSE 1
+#define DAO_MODE_BLOCKS 2 /* f* from key-block lists */
+#define DAO_TILE 64       /* keys per tile of the block lists */
 
 typedef struct {
   const void* q;
@@ -66,6 +81,10 @@ typedef struct {
   const int64_t* cu; /* host, B + 1 entries */
   int B, Hq, Hkv, d;
   int window, n_sink;
+  /* key-block lists (DAO_MODE_BLOCKS only) */
+  const int64_t* blk_ptr; /* [B][Hkv][nqb + 1] */
+  const int64_t* blk_idx;
+  int nqb, block_q;
 } dao_problem;
 
 /* Widen element idx of an input tensor to fp64 (exact for bfloat16). */
@@ -79,10 +98,29 @@ static inline double ld(const void* p, int bf16, int64_t idx) {
   return ((const double*)p)[idx];
 }
 
-/* Key j (<= i) belongs to the key set of row i under the given mode. */
-static inline int key_in_set(int mode, int64_t i, int64_t j, int window, int n_sink) {
+/*
+ * Selected key tiles of row i under the block lists: sel[t] = 1 for every
+ * tile t <= i / 64 in S(i).  sel needs i / 64 + 1 entries.
+ */
+static void block_row_tiles(const dao_problem* P, int b, int g, int64_t i, unsigned char* sel) {
+  const int64_t qb = i / P->block_q;
+  const int64_t diag0 = qb * P->block_q / DAO_TILE; /* first tile of the query block */
+  const int64_t last = i / DAO_TILE;
+  for (int64_t t = 0; t <= last; ++t) sel[t] = (t >= diag0);
+  const int64_t* ptr = P->blk_ptr + ((int64_t)b * P->Hkv + g) * (P->nqb + 1);
+  for (int64_t e = ptr[qb]; e < ptr[qb + 1]; ++e) {
+    const int64_t t = P->blk_idx[e];
+    if (t >= 0 && t < diag0) sel[t] = 1;
+  }
+}
+
+/* Key j (<= i) belongs to the key set of row i under the given mode; for
+ * DAO_MODE_BLOCKS, sel holds the row's selected tiles. */
+static inline int key_in_set(int mode, int64_t i, int64_t j, int window, int n_sink,
+                             const unsigned char* sel) {
   if (j > i) return 0;                 /* causal */
   if (mode == DAO_MODE_DENSE) return 1;
+  if (mode == DAO_MODE_BLOCKS) return sel[j / DAO_TILE];
   return (j < n_sink) || (i - j < window);
 }
 
@@ -91,13 +129,16 @@ static inline int key_in_set(int mode, int64_t i, int64_t j, int window, int n_s
  * key set of `mode`.  Writes o[d]; *m_out / *z_out receive the score max and
  * the normaliser sum_j exp(x_j - m) when non-NULL; w_out (length i+1), when
  * non-NULL, receives the softmax weight of every key j <= i (0 outside the
- * set).  `x` is scratch of at least i+1 doubles.
+ * set).  `x` is scratch of at least i+1 doubles, followed (for the block
+ * lists) by i/64 + 1 bytes of tile flags.
  */
 static void attn_row(const dao_problem* P, int mode, int b, int h, int64_t i,
                      double* o, double* m_out, double* z_out, double* w_out, double* x) {
   const int d = P->d;
   const int G = P->Hq / P->Hkv;
   const int g = h / G;
+  unsigned char* sel = (unsigned char*)(x + i + 1);
+  if (mode == DAO_MODE_BLOCKS) block_row_tiles(P, b, g, i, sel);
   const int64_t base = P->cu[b];
   const double tau = 1.0 / sqrt((double)d);
   const int64_t qoff = ((base + i) * P->Hq + h) * (int64_t)d;
@@ -105,7 +146,7 @@ static void attn_row(const dao_problem* P, int mode, int b, int h, int64_t i,
   /* pass 1: scores over the key set and their max */
   double m = -INFINITY;
   for (int64_t j = 0; j <= i; ++j) {
-    if (!key_in_set(mode, i, j, P->window, P->n_sink)) continue;
+    if (!key_in_set(mode, i, j, P->window, P->n_sink, sel)) continue;
     const int64_t koff = ((base + j) * P->Hkv + g) * (int64_t)d;
     double s = 0.0;
 #pragma omp simd reduction(+ : s)
@@ -117,7 +158,7 @@ static void attn_row(const dao_problem* P, int mode, int b, int h, int64_t i,
   double z = 0.0;
   for (int c = 0; c < d; ++c) o[c] = 0.0;
   for (int64_t j = 0; j <= i; ++j) {
-    if (!key_in_set(mode, i, j, P->window, P->n_sink)) continue;
+    if (!key_in_set(mode, i, j, P->window, P->n_sink, sel)) continue;
     const double p = exp(x[j] - m);
     z += p;
     const int64_t voff = ((base + j) * P->Hkv + g) * (int64_t)d;
@@ -129,7 +170,7 @@ static void attn_row(const dao_problem* P, int mode, int b, int h, int64_t i,
   if (z_out) *z_out = z;
   if (w_out) {
     for (int64_t j = 0; j <= i; ++j)
-      w_out[j] = key_in_set(mode, i, j, P->window, P->n_sink) ? exp(x[j] - m) / z : 0.0;
+      w_out[j] = key_in_set(mode, i, j, P->window, P->n_sink, sel) ? exp(x[j] - m) / z : 0.0;
   }
 }
 
@@ -161,7 +202,7 @@ int dao_attention(const void* q, const void* k, const void* v, int in_bf16,
                   int window, int n_sink, int mode,
                   const int64_t* rows, int64_t n_rows,
                   double* out, double* m_out, double* z_out, int nthreads) {
-  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink, NULL, NULL, 0, 0};
   if (mode != DAO_MODE_DENSE && mode != DAO_MODE_SPARSE) return DAO_ERR_ARG;
   if (mode == DAO_MODE_DENSE) { P.window = 1; P.n_sink = 0; } /* unused by f */
   if (check_problem(&P) != DAO_OK || !out) return DAO_ERR_ARG;
@@ -176,7 +217,7 @@ int dao_attention(const void* q, const void* k, const void* v, int in_bf16,
 #endif
 #pragma omp parallel
   {
-    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1) + (size_t)(Lmax / DAO_TILE + 1));
     if (!x) {
 #pragma omp atomic write
       err = DAO_ERR_NOMEM;
@@ -224,12 +265,12 @@ int dao_attention_weights(const void* q, const void* k, const void* v, int in_bf
                           const int64_t* cu, int B, int Hq, int Hkv, int d,
                           int window, int n_sink, int mode, int b, int h, int64_t i,
                           double* w, double* o) {
-  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink, NULL, NULL, 0, 0};
   if (mode != DAO_MODE_DENSE && mode != DAO_MODE_SPARSE) return DAO_ERR_ARG;
   if (mode == DAO_MODE_DENSE) { P.window = 1; P.n_sink = 0; } /* unused by f */
   if (check_problem(&P) != DAO_OK || !w || !o) return DAO_ERR_ARG;
   if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= cu[b + 1] - cu[b]) return DAO_ERR_ARG;
-  double* x = (double*)malloc(sizeof(double) * (size_t)(i + 1));
+  double* x = (double*)malloc(sizeof(double) * (size_t)(i + 1) + (size_t)(i / DAO_TILE + 1));
   if (!x) return DAO_ERR_NOMEM;
   attn_row(&P, mode, b, h, i, o, NULL, NULL, w, x);
   free(x);
@@ -243,12 +284,11 @@ int dao_attention_weights(const void* q, const void* k, const void* v, int in_bf
  *   delta  [T, Hq, d]  the correction added to each row (optional; zero on
  *                      tail rows, where the dense result replaces the row)
  */
-int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16,
-                        const int64_t* cu, int B, int Hq, int Hkv, int d,
-                        int window, int n_sink, int gamma,
-                        double* out, double* sparse_out, double* delta_out, int nthreads) {
-  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
-  if (check_problem(&P) != DAO_OK || !out || gamma < 1) return DAO_ERR_ARG;
+static int delta_full(const dao_problem* Pp, int smode, int gamma, double* out,
+                      double* sparse_out, double* delta_out, int nthreads) {
+  const dao_problem P = *Pp;
+  const int64_t* cu = P.cu;
+  const int B = P.B, Hq = P.Hq, d = P.d;
   const int64_t T = cu[B];
   const int64_t Lmax = max_len(&P);
   double* sp = sparse_out ? sparse_out : (double*)malloc(sizeof(double) * (size_t)(T * Hq * d + 1));
@@ -262,7 +302,7 @@ int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16
   /* Step 1: A*V <- f*(Q, K, V) for every row of every sequence and head. */
 #pragma omp parallel
   {
-    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1) + (size_t)(Lmax / DAO_TILE + 1));
 #pragma omp for schedule(dynamic, 16)
     for (int64_t it = 0; it < T * Hq; ++it) {
       if (!x) {
@@ -274,7 +314,7 @@ int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16
       const int h = (int)(it % Hq);
       int b = 0;
       while (cu[b + 1] <= t) ++b;
-      attn_row(&P, DAO_MODE_SPARSE, b, h, t - cu[b], sp + it * d, NULL, NULL, NULL, x);
+      attn_row(&P, smode, b, h, t - cu[b], sp + it * d, NULL, NULL, NULL, x);
     }
     free(x);
   }
@@ -283,7 +323,7 @@ int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16
   /* Steps 2-5, per sequence and head. */
 #pragma omp parallel
   {
-    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1) + (size_t)(Lmax / DAO_TILE + 1));
     double* dense = (double*)malloc(sizeof(double) * (size_t)d);
     double* dl = (double*)malloc(sizeof(double) * (size_t)d);
 #pragma omp for schedule(dynamic, 1) collapse(2)
@@ -327,19 +367,26 @@ int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16
   return err;
 }
 
+int dao_delta_attention(const void* q, const void* k, const void* v, int in_bf16,
+                        const int64_t* cu, int B, int Hq, int Hkv, int d,
+                        int window, int n_sink, int gamma,
+                        double* out, double* sparse_out, double* delta_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink, NULL, NULL, 0, 0};
+  if (check_problem(&P) != DAO_OK || !out || gamma < 1) return DAO_ERR_ARG;
+  return delta_full(&P, DAO_MODE_SPARSE, gamma, out, sparse_out, delta_out, nthreads);
+}
+
 /*
  * Delta Attention at selected rows only: for each (b, h, i) the value row i
  * of the full algorithm takes.  A row needs its own sparse key set and the
  * dense and sparse results of its anchor floor(i/gamma)*gamma, so any subset
  * is exact.  out is [n_rows, d]; delta (optional) is [n_rows, d].
  */
-int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in_bf16,
-                             const int64_t* cu, int B, int Hq, int Hkv, int d,
-                             int window, int n_sink, int gamma,
-                             const int64_t* rows, int64_t n_rows,
-                             double* out, double* delta_out, int nthreads) {
-  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
-  if (check_problem(&P) != DAO_OK || !out || !rows || gamma < 1) return DAO_ERR_ARG;
+static int delta_rows(const dao_problem* Pp, int smode, int gamma, const int64_t* rows,
+                      int64_t n_rows, double* out, double* delta_out, int nthreads) {
+  const dao_problem P = *Pp;
+  const int64_t* cu = P.cu;
+  const int B = P.B, Hq = P.Hq, d = P.d;
   const int64_t Lmax = max_len(&P);
   int err = DAO_OK;
 #ifdef _OPENMP
@@ -349,7 +396,7 @@ int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in
 #endif
 #pragma omp parallel
   {
-    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1) + (size_t)(Lmax / DAO_TILE + 1));
     double* sp_i = (double*)malloc(sizeof(double) * (size_t)d);
     double* sp_a = (double*)malloc(sizeof(double) * (size_t)d);
     double* dn_a = (double*)malloc(sizeof(double) * (size_t)d);
@@ -378,8 +425,8 @@ int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in
         continue;
       }
       const int64_t a = (i / gamma) * gamma;
-      attn_row(&P, DAO_MODE_SPARSE, b, h, i, sp_i, NULL, NULL, NULL, x);   /* (A*V)_i */
-      attn_row(&P, DAO_MODE_SPARSE, b, h, a, sp_a, NULL, NULL, NULL, x);   /* (A*V)_a */
+      attn_row(&P, smode, b, h, i, sp_i, NULL, NULL, NULL, x);   /* (A*V)_i */
+      attn_row(&P, smode, b, h, a, sp_a, NULL, NULL, NULL, x);   /* (A*V)_a */
       attn_row(&P, DAO_MODE_DENSE, b, h, a, dn_a, NULL, NULL, NULL, x);    /* (A~V)_a */
       for (int c = 0; c < d; ++c) {
         const double dl = dn_a[c] - sp_a[c];
@@ -393,6 +440,16 @@ int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in
     free(dn_a);
   }
   return err;
+}
+
+int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in_bf16,
+                             const int64_t* cu, int B, int Hq, int Hkv, int d,
+                             int window, int n_sink, int gamma,
+                             const int64_t* rows, int64_t n_rows,
+                             double* out, double* delta_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink, NULL, NULL, 0, 0};
+  if (check_problem(&P) != DAO_OK || !out || !rows || gamma < 1) return DAO_ERR_ARG;
+  return delta_rows(&P, DAO_MODE_SPARSE, gamma, rows, n_rows, out, delta_out, nthreads);
 }
 
 /*
@@ -429,7 +486,7 @@ int dao_delta_attention_variant(const void* q, const void* k, const void* v, int
                                 int window, int n_sink, int gamma, int mode,
                                 double p0, double p1, double p2,
                                 double* out, int nthreads) {
-  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink};
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, window, n_sink, NULL, NULL, 0, 0};
   if (check_problem(&P) != DAO_OK || !out || gamma < 1) return DAO_ERR_ARG;
   if (mode < DAO_CORR_DELTA || mode > DAO_CORR_ABG) return DAO_ERR_ARG;
   const int64_t Lmax = max_len(&P);
@@ -441,7 +498,7 @@ int dao_delta_attention_variant(const void* q, const void* k, const void* v, int
 #endif
 #pragma omp parallel
   {
-    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1) + (size_t)(Lmax / DAO_TILE + 1));
     double* sp = (double*)malloc(sizeof(double) * (size_t)((Lmax + 1) * d));
     double* dl = (double*)malloc(sizeof(double) * (size_t)((Lmax / gamma + 1) * d));
     double* cr = (double*)malloc(sizeof(double) * (size_t)d);
@@ -522,6 +579,119 @@ int dao_delta_attention_variant(const void* q, const void* k, const void* v, int
     free(st);
   }
   return err;
+}
+
+/*
+ * f* given by key-block lists (see the header comment): the lists are CSR,
+ * ptr [B][Hkv][nqb + 1] (offsets into idx, non-decreasing per (b, g)) and
+ * idx (key tile indices local to the sequence); nqb >= ceil(L / block_q)
+ * for every sequence; block_q a positive multiple of 64.
+ */
+static int check_blocks(const dao_problem* P) {
+  if (!P->blk_ptr || P->nqb < 1 || P->block_q < DAO_TILE || P->block_q % DAO_TILE != 0)
+    return DAO_ERR_ARG;
+  for (int b = 0; b < P->B; ++b) {
+    const int64_t L = P->cu[b + 1] - P->cu[b];
+    if ((L + P->block_q - 1) / P->block_q > P->nqb) return DAO_ERR_ARG;
+    for (int g = 0; g < P->Hkv; ++g) {
+      const int64_t* ptr = P->blk_ptr + ((int64_t)b * P->Hkv + g) * (P->nqb + 1);
+      for (int qb = 0; qb < P->nqb; ++qb)
+        if (ptr[qb + 1] < ptr[qb] || ptr[qb] < 0) return DAO_ERR_ARG;
+      if (ptr[P->nqb] > ptr[0] && !P->blk_idx) return DAO_ERR_ARG;
+    }
+  }
+  return DAO_OK;
+}
+
+/* Sparse attention under the block lists for every row (rows == NULL; out
+ * [T, Hq, d]) or for n_rows triples (b, h, i) (out [n_rows, d]). */
+int dao_block_attention(const void* q, const void* k, const void* v, int in_bf16,
+                        const int64_t* cu, int B, int Hq, int Hkv, int d,
+                        const int64_t* blk_ptr, const int64_t* blk_idx, int nqb, int block_q,
+                        const int64_t* rows, int64_t n_rows, double* out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, 1, 0, blk_ptr, blk_idx, nqb, block_q};
+  if (check_problem(&P) != DAO_OK || check_blocks(&P) != DAO_OK || !out) return DAO_ERR_ARG;
+  const int64_t T = cu[B];
+  const int64_t Lmax = max_len(&P);
+  const int64_t n_items = rows ? n_rows : T * Hq;
+  int err = DAO_OK;
+#ifdef _OPENMP
+  if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+  (void)nthreads;
+#endif
+#pragma omp parallel
+  {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(Lmax + 1) + (size_t)(Lmax / DAO_TILE + 1));
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t it = 0; it < n_items; ++it) {
+      if (!x) {
+#pragma omp atomic write
+        err = DAO_ERR_NOMEM;
+        continue;
+      }
+      int b = 0, h;
+      int64_t i;
+      if (rows) {
+        b = (int)rows[3 * it];
+        h = (int)rows[3 * it + 1];
+        i = rows[3 * it + 2];
+      } else {
+        const int64_t t = it / Hq;
+        h = (int)(it % Hq);
+        while (cu[b + 1] <= t) ++b;
+        i = t - cu[b];
+      }
+      if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= cu[b + 1] - cu[b]) {
+#pragma omp atomic write
+        err = DAO_ERR_ARG;
+        continue;
+      }
+      attn_row(&P, DAO_MODE_BLOCKS, b, h, i, out + it * d, NULL, NULL, NULL, x);
+    }
+    free(x);
+  }
+  return err;
+}
+
+/* Algorithm 1 with f* from the block lists: out [T, Hq, d]; sparse and
+ * delta optional as in dao_delta_attention. */
+int dao_block_delta_attention(const void* q, const void* k, const void* v, int in_bf16,
+                              const int64_t* cu, int B, int Hq, int Hkv, int d,
+                              const int64_t* blk_ptr, const int64_t* blk_idx, int nqb,
+                              int block_q, int gamma, double* out, double* sparse_out,
+                              double* delta_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, 1, 0, blk_ptr, blk_idx, nqb, block_q};
+  if (check_problem(&P) != DAO_OK || check_blocks(&P) != DAO_OK || !out || gamma < 1)
+    return DAO_ERR_ARG;
+  return delta_full(&P, DAO_MODE_BLOCKS, gamma, out, sparse_out, delta_out, nthreads);
+}
+
+/* Algorithm 1 with f* from the block lists at selected rows (b, h, i). */
+int dao_block_delta_attention_rows(const void* q, const void* k, const void* v, int in_bf16,
+                                   const int64_t* cu, int B, int Hq, int Hkv, int d,
+                                   const int64_t* blk_ptr, const int64_t* blk_idx, int nqb,
+                                   int block_q, int gamma, const int64_t* rows, int64_t n_rows,
+                                   double* out, double* delta_out, int nthreads) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, 1, 0, blk_ptr, blk_idx, nqb, block_q};
+  if (check_problem(&P) != DAO_OK || check_blocks(&P) != DAO_OK || !out || !rows || gamma < 1)
+    return DAO_ERR_ARG;
+  return delta_rows(&P, DAO_MODE_BLOCKS, gamma, rows, n_rows, out, delta_out, nthreads);
+}
+
+/* Softmax weights of one row (b, h, i) under the block lists (w[j], j <= i). */
+int dao_block_attention_weights(const void* q, const void* k, const void* v, int in_bf16,
+                                const int64_t* cu, int B, int Hq, int Hkv, int d,
+                                const int64_t* blk_ptr, const int64_t* blk_idx, int nqb,
+                                int block_q, int b, int h, int64_t i, double* w, double* o) {
+  dao_problem P = {q, k, v, in_bf16, cu, B, Hq, Hkv, d, 1, 0, blk_ptr, blk_idx, nqb, block_q};
+  if (check_problem(&P) != DAO_OK || check_blocks(&P) != DAO_OK || !w || !o) return DAO_ERR_ARG;
+  if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= cu[b + 1] - cu[b]) return DAO_ERR_ARG;
+  double* x = (double*)malloc(sizeof(double) * (size_t)(i + 1) + (size_t)(i / DAO_TILE + 1));
+  if (!x) return DAO_ERR_NOMEM;
+  attn_row(&P, DAO_MODE_BLOCKS, b, h, i, o, NULL, NULL, w, x);
+  free(x);
+  return DAO_OK;
 }
 
 /* Number of OpenMP threads a parallel region would use (1 without OpenMP). */

@@ -149,3 +149,56 @@ def brute_variant(q, k, v, cu, window, n_sink, gamma, mode, params=(0.0, 0.0, 0.
                 corr = np.repeat(H @ dl, gamma, axis=0)
             res[s0:s0 + Lc, h] = sp[:Lc] + corr
     return res
+
+
+# ---- f* from key-block lists (other sparse bases) ----
+
+def block_mask(L, ptr_bg, idx, block_q):
+    """M[i, j] for one (sequence, kv head): j <= i and tile j//64 is listed for
+    query block i//block_q or lies at or after that block's first tile.
+    ptr_bg: the [nqb + 1] CSR offsets of this (sequence, kv head)."""
+    i = np.arange(L)[:, None]
+    j = np.arange(L)[None, :]
+    nt = -(-L // 64)
+    nq = -(-L // block_q)
+    listed = np.zeros((nq, nt), dtype=bool)
+    for qb in range(nq):
+        diag0 = qb * block_q // 64
+        for t in idx[ptr_bg[qb]:ptr_bg[qb + 1]]:
+            if 0 <= t < diag0:
+                listed[qb, t] = True
+    qb_i = i // block_q
+    tile_j = j // 64
+    return (j <= i) & ((tile_j >= qb_i * block_q // 64) | listed[qb_i, tile_j])
+
+
+def brute_block_parts(q, k, v, cu, ptr, idx, block_q, gamma):
+    """(out, dense AV, sparse A*V) of Algorithm 1 with f* from block lists."""
+    T, Hq, d = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    out = np.zeros((T, Hq, d))
+    dense = np.zeros((T, Hq, d))
+    sparse = np.zeros((T, Hq, d))
+    for b in range(len(cu) - 1):
+        s0, s1 = int(cu[b]), int(cu[b + 1])
+        L = s1 - s0
+        if L == 0:
+            continue
+        Mc, _ = masks(L, 1, 0)
+        Lc = (L // gamma) * gamma
+        anchors = np.arange(0, Lc, gamma)
+        for h in range(Hq):
+            g = h // G
+            Ms = block_mask(L, ptr[b, g], idx, block_q)
+            Q, K, V = q[s0:s1, h], k[s0:s1, g], v[s0:s1, g]
+            X = Q @ K.T / np.sqrt(d)
+            AV = masked_softmax(X, Mc) @ V
+            AsV = masked_softmax(X, Ms) @ V
+            Delta = AV[anchors] - AsV[anchors]
+            o = AV.copy()
+            o[:Lc] = AsV[:Lc] + np.repeat(Delta, gamma, axis=0)
+            out[s0:s1, h] = o
+            dense[s0:s1, h] = AV
+            sparse[s0:s1, h] = AsV
+    return out, dense, sparse
