@@ -177,18 +177,34 @@ def cpu_baseline(wl, q, k, v, target_s=12.0):
     }
 
 
-def time_sparse_only(binding, q, k, v, out, kw, wl, stream, steps):
+def time_sparse_only(binding, q, k, v, out, kw, wl, stream, steps, run=None):
+    """Average time of sparse attention alone (f*) on the same inputs; `run`
+    overrides the sink + window call (another sparse basis)."""
     import torch
-    binding.sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, out=out, **kw)
+    if run is None:
+        run = lambda: binding.sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink,
+                                                  out=out, **kw)
+    run()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(steps):
-        binding.sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, out=out, **kw)
+        run()
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / steps
+
+
+# Key-block-list sparse bases (f* other than sink + window), sized so that a
+# row sees about as many keys as under the 2048-key window with 64 sinks.
+BASES = {
+    "vertical_slash": lambda BL, wl: BL.vertical_slash(wl.seqlens, wl.Hkv, 64, n_vertical=8,
+                                                       n_local=24, slash_offsets=(64, 256),
+                                                       seed=5),
+    "topk": lambda BL, wl: BL.block_topk(wl.seqlens, wl.Hkv, 64, k=33, seed=5),
+    "star": lambda BL, wl: BL.star(wl.seqlens, wl.Hkv, 64, anchor=2048, context=4096),
+}
 
 
 def gamma_sweep(args, wl, binding, q, k, v, kw, dev):
@@ -276,6 +292,9 @@ def main():
     ap.add_argument("--correction-sweep", action="store_true",
                     help="time every step-5 correction variant (one JSON line each) instead "
                          "of the main record")
+    ap.add_argument("--basis", default="streaming", choices=["streaming"] + sorted(BASES),
+                    help="the sparse attention f* Delta corrects: sink + window (the paper's "
+                         "StreamingLLM setting) or key-block lists of another layout")
     ap.add_argument("--path-only", action="store_true",
                     help="time only the Delta path (and the dense baseline unless --no-dense): "
                          "skip the unfused-schedule and sparse-only comparison runs, so a "
@@ -327,15 +346,37 @@ def main():
                max_seqlen=wl.max_seqlen)
     stream = torch.cuda.current_stream(dev)
 
+    # the sparse basis f*: sink + window, or key-block lists
+    basis_cfg = {}
+    if args.basis == "streaming":
+        fused = binding.fused_supported(wl.Hq, wl.Hkv, wl.gamma)
+        run_steps = lambda bits: binding.delta_attn_prefill_steps(q, k, v, out, ws, bits, **pkw)
+        sparse_run = None
+        sparse_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)[0]
+    else:
+        from paper_2505_11254_amd import blocklists as BL
+        bl = BASES[args.basis](BL, wl)
+        bptr, bidx = bl.to(dev)
+        bkw = dict(block_q=bl.block_q, block_ptr=bptr, block_idx=bidx, B=wl.B, cu_seqlens=cu_arg,
+                   max_seqlen=wl.max_seqlen)
+        fused = binding.fused_supported_blocksparse(wl.Hq, wl.Hkv, wl.gamma, bl.block_q)
+        run_steps = lambda bits: binding.delta_attn_prefill_blocksparse(
+            q, k, v, gamma=wl.gamma, out=out, workspace=ws, steps=bits, **bkw)
+        sparse_run = lambda: binding.blocksparse_attn_prefill(q, k, v, out=out, **bkw)
+        sparse_pairs = BL.pair_count(bl, wl.seqlens, wl.Hkv, wl.Hq // wl.Hkv) // wl.Hq
+        basis_cfg = {"basis": args.basis, "block_q": bl.block_q, "list_tiles": int(bl.idx.size),
+                     "avg_keys_per_row": round(sparse_pairs / wl.total_tokens, 1)}
+        log(f"basis {args.basis}: {basis_cfg}")
+
     # the schedule delta_attn_prefill takes for these sizes, one kernel per call
-    fused = binding.fused_supported(wl.Hq, wl.Hkv, wl.gamma)
+    SP = "sparse_window" if args.basis == "streaming" else "sparse_blocks"
     if fused:
         F = binding.STEP_FUSED
         order = [("strided_dense_rows", binding.STEP_DENSE_ROWS | F),
                  ("dense_row_merge", binding.STEP_CORRECT | F),
-                 ("sparse_window", binding.STEP_SPARSE | F)]
+                 (SP, binding.STEP_SPARSE | F)]
     else:
-        order = [("sparse_window", binding.STEP_SPARSE),
+        order = [(SP, binding.STEP_SPARSE),
                  ("strided_dense_rows", binding.STEP_DENSE_ROWS),
                  ("delta_epilogue", binding.STEP_CORRECT)]
 
@@ -345,7 +386,7 @@ def main():
         for i, (_, bits) in enumerate(order):
             if evs is not None:
                 evs[i].record(stream)
-            binding.delta_attn_prefill_steps(q, k, v, out, ws, bits, **pkw)
+            run_steps(bits)
         if evs is not None:
             evs[len(order)].record(stream)
 
@@ -378,7 +419,7 @@ def main():
     # the in-place Delta pass over the output), for comparison
     unfused_ms = None
     if fused and not args.path_only:
-        run_u = lambda: binding.delta_attn_prefill_steps(q, k, v, out, ws, binding.STEP_ALL, **pkw)
+        run_u = lambda: run_steps(binding.STEP_ALL)
         run_u()
         u0 = torch.cuda.Event(enable_timing=True)
         u1 = torch.cuda.Event(enable_timing=True)
@@ -395,12 +436,14 @@ def main():
     # Delta adds on top of the sparse method it corrects
     sparse_only_ms = None
     if not args.path_only:
-        sparse_only_ms = time_sparse_only(binding, q, k, v, out, kw, wl, stream, args.steps)
+        sparse_only_ms = time_sparse_only(binding, q, k, v, out, kw, wl, stream, args.steps,
+                                          run=sparse_run)
         log(f"sparse only: {sparse_only_ms:.3f} ms; "
             f"delta overhead x{ms_per_step / sparse_only_ms:.3f}")
 
     T = wl.total_tokens
-    sp_pairs, dr_pairs, dc_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
+    _, dr_pairs, dc_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
+    sp_pairs = sparse_pairs
     fl = lambda pairs: 4.0 * wl.d * wl.Hq * pairs
     flops = {"sparse": fl(sp_pairs), "dense_rows": fl(dr_pairs), "dense_causal": fl(dc_pairs)}
 
@@ -425,8 +468,7 @@ def main():
         del out_d
 
     per_kernel = {
-        "sparse_window": {"ms": k_ms["sparse_window"],
-                          "useful_tflops": flops["sparse"] / k_ms["sparse_window"] / 1e9},
+        SP: {"ms": k_ms[SP], "useful_tflops": flops["sparse"] / k_ms[SP] / 1e9},
         "strided_dense_rows": {"ms": k_ms["strided_dense_rows"],
                                "useful_tflops": flops["dense_rows"] / k_ms["strided_dense_rows"]
                                / 1e9},
@@ -438,8 +480,8 @@ def main():
     if dense_ms is not None:
         per_kernel["dense_causal"] = {"ms": dense_ms,
                                       "useful_tflops": flops["dense_causal"] / dense_ms / 1e9}
-    dom = max(("sparse_window", "strided_dense_rows"), key=lambda n: per_kernel[n]["ms"])
-    dom_flops = flops["sparse"] if dom == "sparse_window" else flops["dense_rows"]
+    dom = max((SP, "strided_dense_rows"), key=lambda n: per_kernel[n]["ms"])
+    dom_flops = flops["sparse"] if dom == SP else flops["dense_rows"]
     achieved = dom_flops / per_kernel[dom]["ms"] / 1e9
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -447,7 +489,7 @@ def main():
                 "traffic": load_traffic(dom, wl.name)}
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.basis == "streaming":
         log("timing the oracle on a bounded sample of the workload ...")
         cpu = cpu_baseline(wl, q, k, v)
         log(f"cpu baseline: {cpu}")
@@ -466,7 +508,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": dict(wl.describe(), parallelism="single_gpu"),
+        "config": dict(wl.describe(), parallelism="single_gpu", **basis_cfg),
         "schedule": "fused" if fused else "unfused",
         "unfused_ms_per_step": round(unfused_ms, 4) if unfused_ms else None,
         "speedup_vs_dense_causal": round(dense_ms / ms_per_step, 2) if dense_ms else None,

@@ -169,6 +169,58 @@ da_status delta_attn_prefill_correction(const void* q, const void* k, const void
                                         int mode, float p0, float p1, float p2, void* workspace,
                                         size_t workspace_bytes, void* stream);
 
+/*
+ * Delta Attention over other sparse bases (Sec. 3: the correction applies to
+ * any sparse attention f*; Sec. 4 pairs it with StreamingLLM, MInference, HiP
+ * and Star Attention).  f* is given by key-block lists: keys are grouped in
+ * tiles of 64 positions and query rows in blocks of block_q rows, both local
+ * to each sequence.  For sequence b, kv head g and query block qb the list
+ * names the key tiles that the block's rows attend to; the tiles overlapping
+ * the query block itself (tile >= qb*block_q/64) are always attended.  Row i
+ * of a query head of group g then sees
+ *   S(i) = { j <= i : tile(j) listed for (b, g, i/block_q), or
+ *                     tile(j) >= (i/block_q)*block_q/64 },
+ * normalised over S(i) only; Algorithm 1 runs on top unchanged.
+ *
+ * block_ptr: int32 [B][Hkv][nqb + 1], nqb = ceil(max_seqlen / block_q):
+ *   offsets into block_idx; the list of (b, g, qb) is
+ *   block_idx[block_ptr[(b*Hkv + g)*(nqb+1) + qb] .. block_ptr[... + qb + 1]).
+ * block_idx: int32 key tile indices, ascending and unique within each list.
+ *   Entries outside [0, qb*block_q/64) are skipped.
+ * Both arrays are device memory owned by the caller; like cu_seqlens, their
+ * consistency (offsets non-decreasing and inside block_idx, lists ascending
+ * without repeats) is the caller's responsibility: the library cannot check
+ * device-resident values, and violating it is undefined.
+ * block_q must be 64, 128 or 256, and 256/h rows, h the largest power of two
+ * dividing Hq/Hkv (at most 8), must not exceed it (one sparse workgroup's rows
+ * per head lie in one query block); otherwise DA_ERR_UNSUPPORTED.
+ */
+
+/* f* alone under key-block lists, for every row.  cu_seqlens may be NULL (B
+ * sequences of max_seqlen tokens).  Errors as sparse_attn_prefill_varlen,
+ * plus DA_ERR_NULL (no lists), DA_ERR_PARAM (block_q) and DA_ERR_UNSUPPORTED. */
+da_status blocksparse_attn_prefill(const void* q, const void* k, const void* v, void* out,
+                                   const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                   int Hkv, int d, int block_q, const int32_t* block_ptr,
+                                   const int32_t* block_idx, void* stream);
+
+/* Delta Attention with f* under key-block lists.  steps = 0 runs the whole
+ * path in the schedule the library picks (fused when
+ * da_fused_supported_blocksparse()); other values select steps and schedule
+ * as in delta_attn_prefill_steps.  Anchors are never assumed covered: Delta
+ * is formed at every anchor.  workspace: da_workspace_bytes(B, max_seqlen,
+ * Hq, Hkv, d, gamma) bytes. */
+da_status delta_attn_prefill_blocksparse(const void* q, const void* k, const void* v, void* out,
+                                         const int32_t* cu_seqlens, int B, int max_seqlen,
+                                         int Hq, int Hkv, int d, int block_q,
+                                         const int32_t* block_ptr, const int32_t* block_idx,
+                                         int gamma, void* workspace, size_t workspace_bytes,
+                                         void* stream, unsigned steps);
+
+/* As da_fused_supported, with the sparse workgroup's rows per head also
+ * within one query block of block_q rows. */
+int da_fused_supported_blocksparse(int Hq, int Hkv, int gamma, int block_q);
+
 /* Workspace bytes delta_attn_prefill_correction needs (0 if the sizes or mode are invalid). */
 size_t da_workspace_bytes_correction(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma,
                                      int mode);

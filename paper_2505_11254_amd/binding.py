@@ -32,6 +32,8 @@ SIGNATURES = {
     "sparse_attn_prefill_varlen": "pppppiiiiiiip",
     "dense_causal_attn_prefill": "ppppiiiiip",
     "dense_causal_attn_prefill_varlen": "pppppiiiiip",
+    "blocksparse_attn_prefill": "pppppiiiiiippp",
+    "delta_attn_prefill_blocksparse": "pppppiiiiiippipzpu",
 }
 
 
@@ -69,6 +71,8 @@ def load_library(path: str = LIB_PATH):
     lib.da_workspace_bytes_correction.restype = ctypes.c_size_t
     lib.da_fused_supported.argtypes = [ctypes.c_int] * 3
     lib.da_fused_supported.restype = ctypes.c_int
+    lib.da_fused_supported_blocksparse.argtypes = [ctypes.c_int] * 4
+    lib.da_fused_supported_blocksparse.restype = ctypes.c_int
     lib.da_status_string.argtypes = [ctypes.c_int]
     lib.da_status_string.restype = ctypes.c_char_p
     lib.da_last_hip_error.argtypes = []
@@ -205,4 +209,45 @@ def dense_causal_attn_prefill(q, k, v, *, B=None, cu_seqlens=None, max_seqlen=No
     else:
         _call("dense_causal_attn_prefill_varlen", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
               _ptr(cu_seqlens), B_, N, Hq, Hkv, d, st)
+    return out
+
+
+def fused_supported_blocksparse(Hq, Hkv, gamma, block_q) -> bool:
+    """Whether the key-block-list path takes the fused schedule for these sizes."""
+    return bool(load_library().da_fused_supported_blocksparse(Hq, Hkv, gamma, block_q))
+
+
+def _blocks(block_ptr, block_idx):
+    for name, t in (("block_ptr", block_ptr), ("block_idx", block_idx)):
+        if t.dtype != torch.int32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous int32 tensor")
+    return _ptr(block_ptr), _ptr(block_idx)
+
+
+def blocksparse_attn_prefill(q, k, v, *, block_q, block_ptr, block_idx, B=None,
+                             cu_seqlens=None, max_seqlen=None, out=None, stream=None):
+    """Sparse attention whose key sets come from key-block lists, for every row."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    _call("blocksparse_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(cu_seqlens),
+          B_, N, Hq, Hkv, d, block_q, *_blocks(block_ptr, block_idx),
+          _stream(q.device, stream))
+    return out
+
+
+def delta_attn_prefill_blocksparse(q, k, v, *, block_q, block_ptr, block_idx, gamma, B=None,
+                                   cu_seqlens=None, max_seqlen=None, out=None, workspace=None,
+                                   stream=None, steps=0):
+    """Delta Attention with f* from key-block lists; ``steps`` 0 runs the whole path."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    nbytes = workspace_bytes(B_, N, Hq, Hkv, d, gamma)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    wsz = workspace.numel() * workspace.element_size()
+    _call("delta_attn_prefill_blocksparse", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+          _ptr(cu_seqlens), B_, N, Hq, Hkv, d, block_q, *_blocks(block_ptr, block_idx), gamma,
+          _ptr(workspace), wsz, _stream(q.device, stream), steps)
     return out

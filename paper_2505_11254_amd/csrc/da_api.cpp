@@ -53,9 +53,11 @@ int heads_per_block(int G) {
   return h;
 }
 
-int fused_heads_per_block(int G, int gamma) {
-  for (int h = heads_per_block(G); h >= 1; h /= 2)
-    if (G % h == 0 && (kRowsPerWave * (kAttnWaves / h)) % gamma == 0) return h;
+int fused_heads_per_block(int G, int gamma, int max_rows) {
+  for (int h = heads_per_block(G); h >= 1; h /= 2) {
+    const int slab = kRowsPerWave * (kAttnWaves / h);
+    if (G % h == 0 && slab % gamma == 0 && slab <= max_rows) return h;
+  }
   return 0;
 }
 
@@ -106,7 +108,15 @@ struct Problem {
   const int32_t* cu;
   int B, N, Hq, Hkv, d;
   int window, n_sink, gamma;
+  // key-block lists (nullptr: sink + window attention)
+  const int32_t* blk_ptr = nullptr;
+  const int32_t* blk_idx = nullptr;
+  int block_q = 0;
 };
+
+// Rows per query head of one sparse workgroup; with key-block lists they must
+// fit one query block.
+int slab_rows(int hpw) { return kRowsPerWave * (kAttnWaves / hpw); }
 
 // Shape/parameter checks shared by all calls; no HIP call happens here.
 da_status validate(const Problem& P, bool need_window, bool need_gamma) {
@@ -121,6 +131,13 @@ da_status validate(const Problem& P, bool need_window, bool need_gamma) {
   const int64_t rows_per_block = (int64_t)kRowsPerWave * (kAttnWaves / hpw);
   const int64_t blocks = (int64_t)P.B * (P.Hq / hpw) * ((P.N + rows_per_block - 1) / rows_per_block);
   if (blocks > INT32_MAX) return DA_ERR_SHAPE;
+  if (P.blk_ptr || P.blk_idx) {
+    if (!P.blk_ptr || !P.blk_idx) return DA_ERR_NULL;
+    if (P.block_q != 64 && P.block_q != 128 && P.block_q != 256) return DA_ERR_PARAM;
+    if (slab_rows(hpw) > P.block_q) return DA_ERR_UNSUPPORTED;
+    if ((int64_t)P.B * P.Hkv * ((int64_t)(P.N + P.block_q - 1) / P.block_q + 1) > INT32_MAX)
+      return DA_ERR_SHAPE;
+  }
   if (!aligned16(P.q) || !aligned16(P.k) || !aligned16(P.v) || !aligned16(P.out))
     return DA_ERR_ALIGN;
   return DA_OK;
@@ -141,6 +158,18 @@ Args base_args(const Problem& P) {
   a.d = P.d;
   a.window = P.window;
   a.n_sink = P.n_sink;
+  a.cover = (int64_t)P.n_sink + P.window;
+  if (P.blk_ptr) {
+    // the key set is the lists' tiles plus the own query block's, masked
+    // causally: no sink/window test applies, and no anchor is known covered
+    a.blk_ptr = P.blk_ptr;
+    a.blk_idx = P.blk_idx;
+    a.block_q = P.block_q;
+    a.nqb = (P.N + P.block_q - 1) / P.block_q;
+    a.n_sink = INT32_MAX;
+    a.window = 1;
+    a.cover = 0;
+  }
   a.gamma = P.gamma > 0 ? P.gamma : 1;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)P.d));
   a.hpw = heads_per_block(P.Hq / P.Hkv);
@@ -180,7 +209,7 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   if (corr_mode < DA_CORR_DELTA || corr_mode > DA_CORR_ABG) return DA_ERR_PARAM;
   if (!std::isfinite(p0) || !std::isfinite(p1) || !std::isfinite(p2)) return DA_ERR_PARAM;
   if (corr_mode == DA_CORR_EMA && (p0 < 0.f || p0 > 1.f)) return DA_ERR_PARAM;
-  const int fhpw = fused_heads_per_block(P.Hq / P.Hkv, P.gamma);
+  const int fhpw = fused_heads_per_block(P.Hq / P.Hkv, P.gamma, P.blk_ptr ? P.block_q : INT32_MAX);
   const bool can_fuse = fhpw > 0 && corr_mode <= DA_CORR_RECOMPUTE;
   if ((steps & DA_STEP_FUSED) && !can_fuse) return DA_ERR_UNSUPPORTED;
   const bool fused = (steps & DA_STEP_FUSED) || (auto_fuse && can_fuse);
@@ -354,7 +383,40 @@ da_status dense_causal_attn_prefill_varlen(const void* q, const void* k, const v
 
 int da_fused_supported(int Hq, int Hkv, int gamma) {
   if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || gamma < 1) return 0;
-  return da::fused_heads_per_block(Hq / Hkv, gamma) > 0 ? 1 : 0;
+  return da::fused_heads_per_block(Hq / Hkv, gamma, INT32_MAX) > 0 ? 1 : 0;
+}
+
+int da_fused_supported_blocksparse(int Hq, int Hkv, int gamma, int block_q) {
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || gamma < 1) return 0;
+  if (block_q != 64 && block_q != 128 && block_q != 256) return 0;
+  return da::fused_heads_per_block(Hq / Hkv, gamma, block_q) > 0 ? 1 : 0;
+}
+
+da_status blocksparse_attn_prefill(const void* q, const void* k, const void* v, void* out,
+                                   const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                   int Hkv, int d, int block_q, const int32_t* block_ptr,
+                                   const int32_t* block_idx, void* stream) {
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, 1, 0, 1};
+  P.blk_ptr = block_ptr;
+  P.blk_idx = block_idx;
+  P.block_q = block_q;
+  if (!block_ptr || !block_idx) return DA_ERR_NULL;
+  return da::run_plain(P, true, stream);
+}
+
+da_status delta_attn_prefill_blocksparse(const void* q, const void* k, const void* v, void* out,
+                                         const int32_t* cu_seqlens, int B, int max_seqlen,
+                                         int Hq, int Hkv, int d, int block_q,
+                                         const int32_t* block_ptr, const int32_t* block_idx,
+                                         int gamma, void* workspace, size_t workspace_bytes,
+                                         void* stream, unsigned steps) {
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, 1, 0, gamma};
+  P.blk_ptr = block_ptr;
+  P.blk_idx = block_idx;
+  P.block_q = block_q;
+  if (!block_ptr || !block_idx) return DA_ERR_NULL;
+  if (steps == 0u) return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, true);
+  return da::run_delta(P, workspace, workspace_bytes, stream, steps, false);
 }
 
 size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma) {

@@ -32,6 +32,17 @@ struct Args {
   int Hq, Hkv, d;
   int window, n_sink, gamma;
   float scale_log2;   // log2(e) / sqrt(d): scores are exponentiated with exp2
+  // Anchors a < cover have a sparse key set equal to [0, a], so Delta = 0 there
+  // and their groups keep the sparse rows: n_sink + window for sink + window
+  // attention, 0 for key-block lists.
+  int64_t cover;
+
+  // Sparse attention from key-block lists (nullptr: sink + window).  Lists are
+  // CSR per (sequence, kv head, query block of block_q rows): blk_ptr
+  // [B][Hkv][nqb + 1] offsets into blk_idx (key tiles of kKeyTile keys).
+  const int32_t* blk_ptr;
+  const int32_t* blk_idx;
+  int block_q, nqb;
 
   // Workgroup tiling of (query heads x rows): hpw heads of one kv group, each
   // with ppw sub-tiles of 32 rows; hpw * ppw == kAttnWaves.
@@ -75,8 +86,8 @@ size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mo
 int heads_per_block(int G);
 // Heads per workgroup of the fused sparse kernel: the largest power of two
 // dividing G (at most kAttnWaves) whose per-head row slab, 32 * kAttnWaves /
-// hpw rows, is a multiple of gamma; 0 when there is none.
-int fused_heads_per_block(int G, int gamma);
+// hpw rows, is a multiple of gamma and at most max_rows; 0 when there is none.
+int fused_heads_per_block(int G, int gamma, int max_rows);
 
 // Kernel launchers (da_kernels.hip).  Each returns the hipError_t of the launch.
 hipError_t launch_sparse(const Args& a, hipStream_t s);

@@ -187,7 +187,18 @@ void attn_kernel(Args a) {
 
   // ---- key tiles the block visits: [ta0, ta1) then [tb0, tb1)
   int ta0 = 0, ta1 = 0, tb0 = 0, tb1 = 0;
-  if (MODE == kSparse) {
+  // key-block lists: [ta0, ta1) indexes the block's list, then its own query
+  // block's tiles [diag0, last row's tile]
+  int lst0 = 0, diag0 = 0;
+  if (MODE == kSparse && a.blk_ptr) {
+    const int qb = R0 / a.block_q;  // the block's rows lie in one query block
+    const int64_t pi = ((int64_t)b * a.Hkv + g) * (a.nqb + 1) + qb;
+    lst0 = a.blk_ptr[pi];
+    ta1 = max(0, a.blk_ptr[pi + 1] - lst0);
+    diag0 = qb * (a.block_q / kKeyTile);
+    tb0 = diag0;
+    tb1 = max(tb0, bpos_hi / kKeyTile + 1);
+  } else if (MODE == kSparse) {
     const int sink_end = min(a.n_sink, bpos_hi + 1);
     ta1 = (sink_end + kKeyTile - 1) / kKeyTile;
     const int ws = max(0, bpos_lo - a.window + 1);
@@ -234,7 +245,7 @@ void attn_kernel(Args a) {
       for (int u = tid; u < nvec; u += kAttnThreads) {
         const int slot = u / (D / 4), dv = u % (D / 4);
         const int apos = R0 + (slot % per_slab) * a.gamma;
-        if (apos < a_end && (int64_t)apos >= (int64_t)a.n_sink + a.window) {
+        if (apos < a_end && (int64_t)apos >= a.cover) {
           const int hh = hg * a.hpw + slot / per_slab;
           *(f32x4*)(dpre + slot * D + dv * 4) = *(const f32x4*)(
               a.dense + (((int64_t)b * a.Hq + hh) * a.nR_max + apos / a.gamma) * D + dv * 4);
@@ -269,9 +280,10 @@ void attn_kernel(Args a) {
     dma_voff[i] = (int)(r * kv_stride * 2) + (pc ^ LD::vswz(r)) * 16;
   }
   auto dma = [&](int tile, int stage) {
+    if (tile < 0) return;  // a list entry the key set ignores
     const int64_t key0 = (int64_t)tile * kKeyTile;
     const int64_t bytes = (L - key0) * kv_stride * 2;
-    const int nrec = (int)min(bytes, (int64_t)0x7fffffff);
+    const int nrec = (int)max((int64_t)0, min(bytes, (int64_t)0x7fffffff));
     const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(kbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
     const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
@@ -302,12 +314,20 @@ void attn_kernel(Args a) {
     vread[mb] = (4 * half + tr_k) * D + (((4 * mb + 2 * tr_g1 + (tr_m >> 1)) ^ vsw) * 8) +
                 (tr_m & 1) * 4;
 
-  auto tile_at = [&](int it) { return it < n_a ? ta0 + it : tb0 + (it - n_a); };
+  // list entries outside [0, diag0) are not part of the key set (-1: skipped)
+  auto tile_at = [&](int it) -> int {
+    if (it >= n_a) return tb0 + (it - n_a);
+    if (MODE == kSparse && a.blk_ptr) {
+      const int e = a.blk_idx[lst0 + it];
+      return (e >= 0 && e < diag0) ? e : -1;
+    }
+    return ta0 + it;
+  };
 
   // 0: no key of the tile is visible to any row of the wave; 1: every key is
   // visible to every row; 2: mixed, mask per element.
   auto classify = [&](int tile) -> int {
-    if (!wave_has_rows) return 0;
+    if (!wave_has_rows || tile < 0) return 0;
     const int k0 = tile * kKeyTile, k1 = k0 + kKeyTile - 1;
     if (k0 > wpos_hi) return 0;
     if (MODE == kSparse) {
@@ -463,7 +483,7 @@ void attn_kernel(Args a) {
     const float inv = 1.f / lt;
     const bool in_c = row_valid && my_pos < Lc;
     const int anc = in_c ? my_pos - my_pos % a.gamma : 0;
-    const bool open = in_c && (int64_t)anc >= (int64_t)a.n_sink + a.window;
+    const bool open = in_c && (int64_t)anc >= a.cover;
     const bool is_anchor = open && anc == my_pos;
     const bool staged = a.gamma > 1;  // anchor dense rows are in dpre
     const int xslot =
@@ -578,7 +598,7 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
   if (r >= nR) return;
   const bool anchor = r < nA;
   const int pos = anchor ? r * a.gamma : Lc + (r - nA);
-  const bool covered = anchor && (int64_t)pos < (int64_t)a.n_sink + a.window;
+  const bool covered = anchor && (int64_t)pos < a.cover;
   const int h0 = hc * a.head_chunk;
   const int h1 = min(a.Hq, h0 + a.head_chunk);
   const int nh = h1 - h0;

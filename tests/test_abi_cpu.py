@@ -167,3 +167,26 @@ def test_fused_schedule_support_and_step_flags(lib):
     assert call(8) == 3 and call(16) == 3 and call(0) == 3 and call(7 | 16) == 3
     assert call(7 | 8, Hq=6, Hkv=3, gamma=48) == 4   # fused schedule unavailable: rejected
     assert call(1 | 8) == 6 and call(7) == 6          # valid flags: the tiny workspace fails
+
+
+def test_blocksparse_calls_validate_before_the_gpu(lib):
+    sup = lib.da_fused_supported_blocksparse
+    assert sup(32, 8, 64, 64) == 1 and sup(32, 8, 64, 256) == 1
+    assert sup(32, 8, 128, 64) == 0            # 64-row slabs cannot hold 128-row groups
+    assert sup(8, 8, 16, 256) == 1 and sup(8, 8, 16, 128) == 0 and sup(8, 8, 16, 96) == 0
+    f = lib.delta_attn_prefill_blocksparse
+    s = lib.blocksparse_attn_prefill
+
+    def delta(Hq=8, Hkv=2, block_q=64, ptr=FAKE, idx=FAKE, wsz=16, steps=0, gamma=16):
+        return f(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, Hq, Hkv, 128, block_q, ptr, idx, gamma,
+                 FAKE, wsz, None, steps)
+    assert delta(ptr=None) == 1 and delta(idx=None) == 1
+    assert delta(block_q=96) == 3 and delta(block_q=512) == 3 and delta(block_q=32) == 3
+    assert delta(Hq=2, Hkv=2, block_q=64) == 4     # one head per block: 256-row slabs
+    assert delta(Hq=2, Hkv=2, block_q=256) == 6    # allowed; the tiny workspace fails
+    assert delta(steps=16) == 3
+    assert delta(steps=7 | 8, Hq=6, Hkv=3, block_q=256, gamma=48) == 4  # no fused slab fits
+    assert delta() == 6
+    assert s(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 8, 2, 128, 64, None, FAKE, None) == 1
+    assert s(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 8, 2, 128, 100, FAKE, FAKE, None) == 3
+    assert s(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 4, 4, 128, 128, FAKE, FAKE, None) == 4

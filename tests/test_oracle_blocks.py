@@ -190,8 +190,10 @@ BLOCK_MUTANTS = {
                                  "if (t > 0 && t < diag0) sel[t] = 1;"),
     "list_by_query_head": ("if (mode == DAO_MODE_BLOCKS) block_row_tiles(P, b, g, i, sel);",
                            "if (mode == DAO_MODE_BLOCKS) block_row_tiles(P, b, h % P->Hkv, i, sel);"),
-    "query_block_of_one_tile": ("const int64_t qb = i / P->block_q;",
-                                "const int64_t qb = i / DAO_TILE;"),
+    # (each mutant must stay in bounds: a slip in the query-block index itself
+    # would read past the list offsets)
+    "own_block_start_in_query_blocks": ("const int64_t diag0 = qb * P->block_q / DAO_TILE;",
+                                        "const int64_t diag0 = qb;"),
 }
 
 
