@@ -347,9 +347,12 @@ void attn_kernel(Args a) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  auto compute = [&](const uint16_t* ks, int tile, bool masked) {
-    const uint16_t* vs = ks + LD::kElems;
-    f32x16 s0 = f32x16{}, s1 = f32x16{};
+  // S^T of one tile against the wave's rows (register r of lane half h holds
+  // key 8*(r/4) + 4*h + r%4 in s0, that key + 32 in s1); keys outside a row's
+  // key set read -inf when `masked`.
+  auto qk = [&](const uint16_t* ks, int tile, bool masked, f32x16& s0, f32x16& s1) {
+    s0 = f32x16{};
+    s1 = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       const bf16x8 ka = *(const bf16x8*)(ks + kread[kk]);
@@ -357,6 +360,15 @@ void attn_kernel(Args a) {
       s0 = mfma32(ka, qf[kk], s0);
       s1 = mfma32(kb, qf[kk], s1);
     }
+    // issue the K reads four MFMAs ahead of their use, so the matrix phase is
+    // not paced by LDS latency
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int i = 0; i < D / 8 - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     // accumulator register r of lane half h holds key 8*(r/4) + 4*h + r%4
     if (masked) {
       const int kbase_t = tile * kKeyTile + 4 * half;
@@ -373,6 +385,12 @@ void attn_kernel(Args a) {
         s1[r] = ok1 ? s1[r] : -INFINITY;
       }
     }
+  };
+
+  // Online-softmax update with one tile's scores: moves the reference max
+  // when needed (rescaling O and l), adds the tile's weights to l and
+  // returns them as bf16 P^T fragments.
+  auto softmax = [&](const f32x16& s0, const f32x16& s1, bf16x8* pf) {
     // row max over the 32 scores of this lane (a tree of 3-input max), then
     // across the lane pair l, l^32 that shares the row
     float t3[11];
@@ -411,7 +429,6 @@ void attn_kernel(Args a) {
     }
     // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block t/2.
     // The normaliser sums the bf16 weights the MFMA multiplies (dot2 with 1,1).
-    bf16x8 pf[4];
     pf[0] = __builtin_convertvector(p0.lo, bf16x8);
     pf[1] = __builtin_convertvector(p0.hi, bf16x8);
     pf[2] = __builtin_convertvector(p1.lo, bf16x8);
@@ -423,6 +440,10 @@ void attn_kernel(Args a) {
       l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 4, 5), ones2, l, false);
       l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 6, 7), ones2, l, false);
     }
+  };
+
+  // O^T += V^T P^T for one tile.
+  auto pv = [&](const uint16_t* vs, const bf16x8* pf) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
 #pragma unroll
@@ -433,6 +454,22 @@ void attn_kernel(Args a) {
         o[mb] = mfma32(__builtin_bit_cast(bf16x8, both), pf[t], o[mb]);
       }
     }
+    // V^T reads (two per MFMA) four MFMAs ahead of their use
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < D / 8 - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  };
+
+  auto compute = [&](const uint16_t* ks, int tile, bool masked) {
+    f32x16 s0, s1;
+    bf16x8 pf[4];
+    qk(ks, tile, masked, s0, s1);
+    softmax(s0, s1, pf);
+    pv(ks + LD::kElems, pf);
   };
 
   // ---- main loop over a ring of NS LDS stages, one barrier per tile.  Step
