@@ -221,7 +221,7 @@ def gamma_sweep(args, wl, binding, q, k, v, kw, dev):
         ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
         run = lambda: binding.delta_attn_prefill(q, k, v, window=w2.window, n_sink=w2.n_sink,
                                                  gamma=g, out=out, workspace=ws, **kw)
-        for _ in range(args.warmup):
+        for _ in range(args.warmup if args.warmup is not None else 3):
             run()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -260,7 +260,7 @@ def correction_sweep(args, wl, binding, q, k, v, kw, dev):
         run = lambda: binding.delta_attn_prefill_correction(
             q, k, v, window=wl.window, n_sink=wl.n_sink, gamma=wl.gamma, mode=mode,
             params=params, out=out, workspace=ws, **kw)
-        for _ in range(args.warmup):
+        for _ in range(args.warmup if args.warmup is not None else 3):
             run()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
@@ -281,7 +281,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warmup steps (default: at least 2, and enough for 0.5 s of "
+                         "work so the clocks settle on short steps)")
     ap.add_argument("--workload", default=None)
     ap.add_argument("--dense-steps", type=int, default=1)
     ap.add_argument("--no-dense", action="store_true")
@@ -390,9 +392,16 @@ def main():
         if evs is not None:
             evs[len(order)].record(stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    if args.warmup is not None:
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+    else:
+        args.warmup, t0 = 0, time.perf_counter()
+        while args.warmup < 2 or time.perf_counter() - t0 < 0.5:
+            step()
+            torch.cuda.synchronize()
+            args.warmup += 1
     log(f"warmup done ({args.warmup} steps)")
 
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(order) + 1)]
