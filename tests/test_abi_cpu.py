@@ -190,3 +190,22 @@ def test_blocksparse_calls_validate_before_the_gpu(lib):
     assert s(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 8, 2, 128, 64, None, FAKE, None) == 1
     assert s(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 8, 2, 128, 100, FAKE, FAKE, None) == 3
     assert s(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, 4, 4, 128, 128, FAKE, FAKE, None) == 4
+
+
+def test_rejected_calls_leave_out_untouched(lib):
+    """Validation fails before any access: host buffers standing in for the
+    tensors keep their bytes (no HIP call and no write happens)."""
+    import numpy as np
+    buf = np.full(4096, 0x5A, dtype=np.uint8)
+    base = buf.ctypes.data
+    p = base + (-base) % 16  # 16-byte aligned inside the buffer
+    before = buf.copy()
+    # unsupported head size, misaligned k, bad window, too small a workspace
+    assert lib.delta_attn_prefill(p, p, p, p, 1, 8, 2, 64, 96, 16, 4, 16, p, 1 << 20, None) == 4
+    assert lib.delta_attn_prefill(p, p + 4, p, p, 1, 8, 2, 64, 128, 16, 4, 16, p, 1 << 20,
+                                  None) == 5
+    assert lib.delta_attn_prefill(p, p, p, p, 1, 8, 2, 64, 128, 0, 4, 16, p, 1 << 20, None) == 3
+    assert lib.delta_attn_prefill(p, p, p, p, 1, 8, 2, 64, 128, 16, 4, 16, p, 64, None) == 6
+    assert lib.sparse_attn_prefill(p, p, p, p, 1, 8, 3, 64, 128, 16, 4, None) == 2
+    assert lib.dense_causal_attn_prefill(p, p, p, p, 0, 8, 2, 64, 128, None) == 2
+    assert np.array_equal(buf, before)
