@@ -463,6 +463,8 @@ def main():
         out_d = torch.empty_like(q)
         tiny = generate(WORKLOADS["tiny_n1024_d64"], device=dev)
         binding.dense_causal_attn_prefill(*tiny[:3])  # load the code object
+        if flops["dense_causal"] < 2e15:  # under ~2 s: one untimed launch settles the clocks
+            binding.dense_causal_attn_prefill(q, k, v, out=out_d, **kw)
         torch.cuda.synchronize()
         de0 = torch.cuda.Event(enable_timing=True)
         de1 = torch.cuda.Event(enable_timing=True)
