@@ -485,23 +485,31 @@ void attn_kernel(Args a) {
   for (int p = 0; p < NS - 1; ++p)
     if (p < n_iter) dma(tile_at(p), p);
   constexpr int kLoadsPerTile = 2 * RPW;  // vmcnt entries one tile's DMA adds per wave
-  for (int it = 0; it < n_iter; ++it) {
-    const int ahead = min(NS - 2, n_iter - 1 - it);  // later tiles already in flight
-    if (NS >= 4 && ahead >= 2)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kLoadsPerTile) & 15) | (((2 * kLoadsPerTile) >> 4) << 14));
-    else if (NS >= 3 && ahead >= 1)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | (kLoadsPerTile & 15) | ((kLoadsPerTile >> 4) << 14));
-    else
-      __builtin_amdgcn_s_waitcnt(0x0F70);
-    __syncthreads();
-    if (it + NS - 1 < n_iter) dma(tile_at(it + NS - 1), (it + NS - 1) % NS);
-    const int tile = tile_at(it);
-    const int cls = classify(tile);
-    const uint16_t* ks = smem + (it % NS) * LD::stageElems;
-    if (cls == 1)
-      compute(ks, tile, false);
-    else if (cls == 2)
-      compute(ks, tile, true);
+  // The loop is unrolled by the ring depth so each step's stage is a constant:
+  // the LDS operand addresses are then a loop-invariant per-lane register plus
+  // an immediate offset, with no address arithmetic per tile.
+  for (int it0 = 0; it0 < n_iter; it0 += NS) {
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int it = it0 + st;
+      if (it >= n_iter) break;
+      const int ahead = min(NS - 2, n_iter - 1 - it);  // later tiles already in flight
+      if (NS >= 4 && ahead >= 2)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kLoadsPerTile) & 15) | (((2 * kLoadsPerTile) >> 4) << 14));
+      else if (NS >= 3 && ahead >= 1)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | (kLoadsPerTile & 15) | ((kLoadsPerTile >> 4) << 14));
+      else
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+      __syncthreads();
+      if (it + NS - 1 < n_iter) dma(tile_at(it + NS - 1), (st + NS - 1) % NS);
+      const int tile = tile_at(it);
+      const int cls = classify(tile);
+      const uint16_t* ks = smem + st * LD::stageElems;
+      if (cls == 1)
+        compute(ks, tile, false);
+      else if (cls == 2)
+        compute(ks, tile, true);
+    }
   }
 
   // ---- epilogue: output register r of block mb is dim 32*mb + 8*(r/4) + 4*half + r%4
