@@ -369,17 +369,25 @@ void attn_kernel(Args a) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    // accumulator register r of lane half h holds key 8*(r/4) + 4*h + r%4
+    // accumulator register r of lane half h holds key kbase_t + o with the
+    // constant offset o = 8*(r/4) + r%4 (+32 in s1); the tests compare o
+    // against per-lane bounds: causal o <= my_pos - kbase_t, window
+    // o > my_pos - kbase_t - window, sink o < n_sink - kbase_t
     if (masked) {
       const int kbase_t = tile * kKeyTile + 4 * half;
+      const int lim_c = my_pos - kbase_t;
+      // (64-bit: the window may be as large as INT_MAX; every offset is >= 0,
+      // so a bound clamped at -1 admits the whole tile, as such a window does)
+      const int lim_w = (int)max((int64_t)lim_c - (int64_t)a.window, (int64_t)-1);
+      const int lim_s = a.n_sink - kbase_t;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int j0 = kbase_t + 8 * (r >> 2) + (r & 3);
-        const int j1 = j0 + 32;
-        bool ok0 = j0 <= my_pos, ok1 = j1 <= my_pos;
+        const int o0 = 8 * (r >> 2) + (r & 3);
+        const int o1 = o0 + 32;
+        bool ok0 = o0 <= lim_c, ok1 = o1 <= lim_c;
         if (MODE == kSparse) {
-          ok0 = ok0 && (j0 < a.n_sink || my_pos - j0 < a.window);
-          ok1 = ok1 && (j1 < a.n_sink || my_pos - j1 < a.window);
+          ok0 = ok0 && (o0 < lim_s || o0 > lim_w);
+          ok1 = ok1 && (o1 < lim_s || o1 > lim_w);
         }
         s0[r] = ok0 ? s0[r] : -INFINITY;
         s1[r] = ok1 ? s1[r] : -INFINITY;

@@ -61,6 +61,7 @@ SMALL = [
     ((200,), 2, 2, 64, 16, 4, 512),               # gamma > N: the whole sequence is tail
     ((2500,), 6, 3, 128, 200, 300, 48),           # GQA 2, sinks wider than the window
     ((130, 70), 2, 1, 128, 33, 1, 7),             # odd gamma, short sequences
+    ((300,), 4, 1, 128, 2 ** 31 - 1, 0, 16),      # the largest window: sparse = dense
 ]
 
 
