@@ -216,3 +216,27 @@ def test_workload_ragged_b4_sampled():
 @pytest.mark.timeout(900)
 def test_workload_llama8b_1m_sampled():
     _workload_case("llama8b_layer_1m")
+
+
+@pytest.mark.timeout(600)
+def test_interleaved_xcd_map_at_scale():
+    """Head groups that do not split evenly over the 8 XCDs (here 4 groups of one
+    head) take the interleaved-chunk block map, which only engages on grids of
+    at least 512 blocks: 64K tokens give 1024 sparse blocks and a strided grid
+    of the same order; checked on sampled rows, sparse and Delta outputs."""
+    from paper_2505_11254_amd.inputs import random_qkv
+    L, Hq, Hkv, d, w, s, gamma = 65536, 4, 4, 64, 512, 16, 32
+    q, k, v, cu = random_qkv((L,), Hq, Hkv, d, seed=41, device=DEV)
+    out = B().delta_attn_prefill(q, k, v, window=w, n_sink=s, gamma=gamma)
+    sp = B().sparse_attn_prefill(q, k, v, window=w, n_sink=s)
+    torch.cuda.synchronize()
+    rows = sample_rows((L,), Hq, w, s, gamma, n_random=160, seed=5)
+    got, got_sp = gather_rows(out, [0, L], rows), gather_rows(sp, [0, L], rows)
+    bits = [to_oracle_bits(x) for x in (q, k, v)]
+    del q, k, v, out, sp
+    cu64 = np.asarray([0, L], dtype=np.int64)
+    ref = oracle.delta_attention_rows(*bits, cu64, window=w, n_sink=s, gamma=gamma, rows=rows)
+    ref_sp = oracle.attention(*bits, cu64, mode=oracle.MODE_SPARSE, window=w, n_sink=s, rows=rows)
+    assert_parity(got, ref, f"interleaved map, delta path ({len(rows)} rows)")
+    assert_parity(got_sp, ref_sp, "interleaved map, sparse kernel")
+
