@@ -254,6 +254,27 @@ da_status dense_causal_attn_prefill_varlen(const void* q, const void* k, const v
  */
 size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma);
 
+/*
+ * Checks, on the GPU, the device-resident inputs the other calls take on
+ * trust, and waits for the answer (this call synchronises `stream`; it is a
+ * debugging aid, not for the hot path):
+ *   cu_seqlens (when not NULL, B+1 entries): starts at 0, is non-decreasing,
+ *     and no length exceeds max_seqlen;
+ *   block_ptr / block_idx (when block_ptr is not NULL; the layout of
+ *     delta_attn_prefill_blocksparse with nqb = ceil(max_seqlen / block_q),
+ *     block_idx holding block_nnz entries): per (sequence, kv head) the
+ *     offsets lie in [0, block_nnz] and do not decrease, and every list is
+ *     strictly ascending.
+ * `result` (device, int32, 4-byte aligned, caller-owned) receives the number
+ * of violations.  Returns DA_OK when there are none and DA_ERR_PARAM when
+ * there are some; DA_ERR_NULL without result or without anything to check,
+ * DA_ERR_SHAPE / DA_ERR_PARAM for bad sizes or block_q, DA_ERR_HIP when a HIP
+ * call fails.  The arrays must have the sizes stated above.
+ */
+da_status da_check_inputs(const int32_t* cu_seqlens, int B, int max_seqlen, int Hkv, int block_q,
+                          const int32_t* block_ptr, const int32_t* block_idx, int64_t block_nnz,
+                          int32_t* result, void* stream);
+
 /* Static, NUL-terminated name of a status code. */
 const char* da_status_string(da_status s);
 

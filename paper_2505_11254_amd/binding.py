@@ -34,6 +34,7 @@ SIGNATURES = {
     "dense_causal_attn_prefill_varlen": "pppppiiiiip",
     "blocksparse_attn_prefill": "pppppiiiiiippp",
     "delta_attn_prefill_blocksparse": "pppppiiiiiippipzpu",
+    "da_check_inputs": "piiiipplpp",
 }
 
 
@@ -60,7 +61,7 @@ def load_library(path: str = LIB_PATH):
                            "(hipcc for gfx950); there is no fallback implementation")
     lib = ctypes.CDLL(path)
     codes = {"p": ctypes.c_void_p, "i": ctypes.c_int, "z": ctypes.c_size_t,
-             "u": ctypes.c_uint, "f": ctypes.c_float}
+             "u": ctypes.c_uint, "f": ctypes.c_float, "l": ctypes.c_int64}
     for name, sig in SIGNATURES.items():
         f = getattr(lib, name)
         f.argtypes = [codes[c] for c in sig]
@@ -251,3 +252,23 @@ def delta_attn_prefill_blocksparse(q, k, v, *, block_q, block_ptr, block_idx, ga
           _ptr(cu_seqlens), B_, N, Hq, Hkv, d, block_q, *_blocks(block_ptr, block_idx), gamma,
           _ptr(workspace), wsz, _stream(q.device, stream), steps)
     return out
+
+
+def check_inputs(*, max_seqlen, B=None, cu_seqlens=None, Hkv=None, block_q=None,
+                 block_ptr=None, block_idx=None, stream=None):
+    """Count violations of the rules cu_seqlens and key-block lists must follow
+    (see da_check_inputs); synchronises the stream.  Returns the count."""
+    import torch as _t
+    dev = (cu_seqlens if cu_seqlens is not None else block_ptr).device
+    if B is None:
+        B = cu_seqlens.numel() - 1
+    result = _t.zeros(1, dtype=_t.int32, device=dev)
+    nnz = block_idx.numel() if block_idx is not None else 0
+    lib = load_library()
+    rc = lib.da_check_inputs(_ptr(cu_seqlens), B, max_seqlen, Hkv or 0, block_q or 0,
+                             _ptr(block_ptr), _ptr(block_idx), nnz, _ptr(result),
+                             _stream(dev, stream))
+    if rc not in (0, 3):
+        raise DeltaAttnError("da_check_inputs", rc, lib.da_last_hip_error())
+    return int(result.item())
+

@@ -425,6 +425,32 @@ size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gam
   return p.bytes;
 }
 
+da_status da_check_inputs(const int32_t* cu_seqlens, int B, int max_seqlen, int Hkv,
+                          int block_q, const int32_t* block_ptr, const int32_t* block_idx,
+                          int64_t block_nnz, int32_t* result, void* stream) {
+  if (!result || (!cu_seqlens && !block_ptr)) return DA_ERR_NULL;
+  if (B < 1 || max_seqlen < 1) return DA_ERR_SHAPE;
+  int nqb = 0;
+  if (block_ptr) {
+    if (!block_idx && block_nnz > 0) return DA_ERR_NULL;
+    if (Hkv < 1 || block_nnz < 0) return DA_ERR_SHAPE;
+    if (block_q != 64 && block_q != 128 && block_q != 256) return DA_ERR_PARAM;
+    nqb = (max_seqlen + block_q - 1) / block_q;
+  }
+  if (((uintptr_t)result & 3u) != 0) return DA_ERR_ALIGN;
+  da_status st = da::check_device();
+  if (st != DA_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = da::launch_check_inputs(cu_seqlens, B, max_seqlen, block_ptr, block_idx,
+                                         block_nnz, Hkv, nqb, result, s);
+  if (e != hipSuccess) return da::fail_hip(e);
+  int32_t host = 0;
+  e = hipMemcpyAsync(&host, result, sizeof host, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return da::fail_hip(e);
+  return host == 0 ? DA_OK : DA_ERR_PARAM;
+}
+
 const char* da_status_string(da_status s) {
   switch (s) {
     case DA_OK: return "DA_OK";

@@ -95,5 +95,8 @@ hipError_t launch_dense(const Args& a, hipStream_t s);
 hipError_t launch_dense_rows(const Args& a, hipStream_t s);
 hipError_t launch_delta_epilogue(const Args& a, hipStream_t s);
 hipError_t launch_correction(const Args& a, hipStream_t s);
+hipError_t launch_check_inputs(const int32_t* cu, int B, int max_seqlen, const int32_t* bptr,
+                              const int32_t* bidx, int64_t nnz, int Hkv, int nqb,
+                              int32_t* result, hipStream_t s);
 
 }  // namespace da

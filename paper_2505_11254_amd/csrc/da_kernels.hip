@@ -835,6 +835,50 @@ __global__ __launch_bounds__(kEpiThreads) void corr_apply_kernel(Args a) {
   }
 }
 
+// Counts violations of what the other kernels take on trust in device-resident
+// inputs (one workgroup; a debugging aid, not on the hot path):
+//   cu_seqlens: starts at 0, non-decreasing, every length <= max_seqlen;
+//   key-block lists, per (sequence, kv head): offsets inside [0, nnz] and
+//   non-decreasing over the query blocks, each list strictly ascending.
+// Every load is guarded by the checks before it, so malformed offsets are
+// counted, never followed out of bounds.
+__global__ __launch_bounds__(256) void check_inputs_kernel(const int32_t* cu, int B, int max_seqlen,
+                                                           const int32_t* bptr,
+                                                           const int32_t* bidx, int64_t nnz,
+                                                           int Hkv, int nqb, int32_t* result) {
+  __shared__ int32_t red[256];
+  int32_t bad = 0;
+  const int tid = threadIdx.x;
+  if (cu) {
+    if (tid == 0 && cu[0] != 0) ++bad;
+    for (int i = tid; i < B; i += 256) {
+      const int64_t len = (int64_t)cu[i + 1] - cu[i];
+      if (len < 0 || len > max_seqlen) ++bad;
+    }
+  }
+  if (bptr) {
+    for (int64_t row = tid; row < (int64_t)B * Hkv; row += 256) {
+      const int32_t* p = bptr + row * (nqb + 1);
+      bool ok = p[0] >= 0 && (int64_t)p[nqb] <= nnz;
+      for (int qb = 0; qb < nqb; ++qb) ok = ok && p[qb + 1] >= p[qb];
+      if (!ok) {
+        ++bad;
+        continue;
+      }
+      for (int qb = 0; qb < nqb; ++qb)
+        for (int64_t e = (int64_t)p[qb] + 1; e < p[qb + 1]; ++e)
+          if (bidx[e] <= bidx[e - 1]) ++bad;
+    }
+  }
+  red[tid] = bad;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (tid < w) red[tid] += red[tid + w];
+    __syncthreads();
+  }
+  if (tid == 0) *result = red[0];
+}
+
 template <int MODE>
 hipError_t launch_attn(const Args& a, hipStream_t s, int64_t nblocks) {
   if (nblocks <= 0) return hipSuccess;
@@ -846,6 +890,14 @@ hipError_t launch_attn(const Args& a, hipStream_t s, int64_t nblocks) {
 }
 
 }  // namespace
+
+hipError_t launch_check_inputs(const int32_t* cu, int B, int max_seqlen, const int32_t* bptr,
+                              const int32_t* bidx, int64_t nnz, int Hkv, int nqb,
+                              int32_t* result, hipStream_t s) {
+  hipLaunchKernelGGL(check_inputs_kernel, dim3(1), dim3(256), 0, s, cu, B, max_seqlen, bptr, bidx,
+                     nnz, Hkv, nqb, result);
+  return hipGetLastError();
+}
 
 hipError_t launch_sparse(const Args& a, hipStream_t s) {
   return launch_attn<kSparse>(a, s, (int64_t)a.B * a.n_hgroups * a.n_rtiles);

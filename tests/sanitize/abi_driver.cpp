@@ -20,6 +20,11 @@ hipError_t launch_dense(const Args&, hipStream_t) { ++g_launched; return hipSucc
 hipError_t launch_dense_rows(const Args&, hipStream_t) { ++g_launched; return hipSuccess; }
 hipError_t launch_delta_epilogue(const Args&, hipStream_t) { ++g_launched; return hipSuccess; }
 hipError_t launch_correction(const Args&, hipStream_t) { ++g_launched; return hipSuccess; }
+hipError_t launch_check_inputs(const int32_t*, int, int, const int32_t*, const int32_t*, int64_t,
+                               int, int, int32_t*, hipStream_t) {
+  ++g_launched;
+  return hipSuccess;
+}
 }  // namespace da
 
 static int failures = 0;
@@ -54,6 +59,11 @@ int main() {
   expect(delta_attn_prefill_blocksparse(p, p, p, p, nullptr, 1, 64, 8, 2, 128, 64, nullptr, lists, 16, p, 1 << 20, nullptr, 0), DA_ERR_NULL, "no lists");
   expect(sparse_attn_prefill(p, p, p, p, 1, 8, 2, 64, 128, 16, -2, nullptr), DA_ERR_PARAM, "sparse sinks");
   expect(dense_causal_attn_prefill(p, p, p, p, 1, 8, 2, 64, 256, nullptr), DA_ERR_UNSUPPORTED, "dense d 256");
+  int32_t* rp = (int32_t*)p;
+  expect(da_check_inputs(nullptr, 2, 64, 2, 64, nullptr, nullptr, 0, rp, nullptr), DA_ERR_NULL, "check: nothing");
+  expect(da_check_inputs(lists, 2, 64, 2, 64, nullptr, nullptr, 0, nullptr, nullptr), DA_ERR_NULL, "check: result");
+  expect(da_check_inputs(lists, 0, 64, 2, 64, nullptr, nullptr, 0, rp, nullptr), DA_ERR_SHAPE, "check: B");
+  expect(da_check_inputs(nullptr, 1, 64, 2, 100, lists, lists, 8, rp, nullptr), DA_ERR_PARAM, "check: block_q");
   expect(da_workspace_bytes(1, 64, 8, 3, 128, 16) == 0 ? 0 : 1, 0, "workspace of a bad shape");
   expect(da_workspace_bytes(1, 1 << 20, 32, 8, 128, 64) % 256 == 0 ? 0 : 1, 0, "workspace alignment");
   expect(da_fused_supported(32, 8, 64), 1, "fused 64");

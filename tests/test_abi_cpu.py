@@ -209,3 +209,14 @@ def test_rejected_calls_leave_out_untouched(lib):
     assert lib.sparse_attn_prefill(p, p, p, p, 1, 8, 3, 64, 128, 16, 4, None) == 2
     assert lib.dense_causal_attn_prefill(p, p, p, p, 0, 8, 2, 64, 128, None) == 2
     assert np.array_equal(buf, before)
+
+
+def test_check_inputs_validates_its_arguments(lib):
+    f = lib.da_check_inputs
+    assert f(FAKE, 2, 128, 2, 64, None, None, 0, None, None) == 1         # no result buffer
+    assert f(None, 2, 128, 2, 64, None, None, 0, FAKE, None) == 1         # nothing to check
+    assert f(FAKE, 0, 128, 2, 64, None, None, 0, FAKE, None) == 2         # B < 1
+    assert f(None, 1, 128, 2, 96, FAKE, FAKE, 10, FAKE, None) == 3        # block_q
+    assert f(None, 1, 128, 0, 64, FAKE, FAKE, 10, FAKE, None) == 2        # Hkv < 1
+    assert f(None, 1, 128, 2, 64, FAKE, None, 10, FAKE, None) == 1        # entries without idx
+    assert f(FAKE, 1, 128, 2, 64, None, None, 0, FAKE + 2, None) == 5     # result alignment
