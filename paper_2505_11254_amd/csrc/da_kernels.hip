@@ -1,7 +1,8 @@
 // da_kernels.hip -- gfx950 (CDNA4) kernels of the Delta Attention prefill.
 //
 // Delta Attention (arXiv 2505.11254, Algorithm 1) runs three steps:
-//   1. sparse attention A*V for every query (StreamingLLM sinks + window),
+//   1. sparse attention A*V for every query (StreamingLLM sinks + window, or
+//      key tiles from per-query-block lists for other sparse bases),
 //   2. dense causal attention A~V for every gamma-th query row (Eq. 4),
 //   3. Delta = A~V - (A*V) at those rows, added to the gamma rows each covers
 //      (Eq. 6); rows after the last whole group are computed densely
@@ -36,7 +37,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 enum Mode { kSparse = 0, kDense = 1, kDenseRows = 2 };
 
@@ -485,7 +485,8 @@ void attn_kernel(Args a) {
   // still be in flight), meets the other waves at the barrier (after which
   // tile it is in LDS for everyone and nobody reads stage (it-1) % NS any
   // more), starts the DMA of tile it+NS-1 into that stage, then computes
-  // tile it.  LDS starts zeroed so a key the DMA leaves untouched is finite.
+  // tile it.  LDS starts zeroed, so no stage ever holds non-finite bits (keys
+  // past the sequence end arrive as zeros from the DMA).
   for (int i = tid; i < NS * LD::stageElems / 8; i += kAttnThreads)
     *(u32x4*)(smem + 8 * i) = u32x4{0u, 0u, 0u, 0u};
   __syncthreads();
@@ -531,8 +532,9 @@ void attn_kernel(Args a) {
     // prologue staged in LDS and leaves it there for the group's other rows,
     // which store bf16(sparse + Delta), one rounding.  Anchor rows store the
     // dense row, tail rows (past the last whole group) the dense row too;
-    // groups whose anchor a < n_sink + window have Delta = 0 exactly and keep
-    // the sparse row untouched.  Recompute (fuse 2) replaces anchors only.
+    // groups whose anchor lies below a.cover (a < n_sink + window: its sparse
+    // key set is all of [0, a]) have Delta = 0 exactly and keep the sparse row
+    // untouched.  Recompute (fuse 2) replaces anchors only.
     const float inv = 1.f / lt;
     const bool in_c = row_valid && my_pos < Lc;
     const int anc = in_c ? my_pos - my_pos % a.gamma : 0;
@@ -622,8 +624,9 @@ void attn_kernel(Args a) {
 //   anchor row a = r*gamma:  Delta = dense - sparse(a) in fp32, out[a] = dense,
 //                            out[i] += Delta for i = a+1 .. a+gamma-1;
 //   tail row:                out[row] = dense.
-// An anchor with a < n_sink + window sees all keys 0..a in its sparse set, so
-// its Delta is exactly zero and the block leaves its rows untouched.
+// An anchor below a.cover (a < n_sink + window: all keys 0..a are in its
+// sparse set) has Delta exactly zero and the block leaves its rows untouched;
+// with key-block lists no anchor is assumed covered (cover = 0).
 // Epilogue modes: the Delta correction itself; "recompute" (Eq. 5: the dense
 // row replaces the sparse one at anchors only); merge only (Delta_i into
 // dbuf for the other correction variants, tail rows into out); or, for the
