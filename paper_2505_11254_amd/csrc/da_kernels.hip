@@ -395,59 +395,75 @@ void attn_kernel(Args a) {
     }
   };
 
-  // Online-softmax update with one tile's scores: moves the reference max
-  // when needed (rescaling O and l), adds the tile's weights to l and
-  // returns them as bf16 P^T fragments.
+  // Online-softmax update with one tile's scores: adds the tile's weights to
+  // l and returns them as bf16 P^T fragments, moving the reference max first
+  // when it has to.
+  //
+  // The reference max m lags the true running max: weights are taken against
+  // the current m, and only if some lane's share of the tile's weight sum
+  // exceeds 2^13 (or no reference exists yet) does the wave take the row max
+  // of the tile.  m then moves to it when a score exceeds m by more than 2^8
+  // after exponentiation (rescaling O and l), and the weights are taken
+  // again.  Every weight stays below 2^13 (harmless in fp32 and bf16): a lane
+  // whose scores all lie within 2^8 of m sums at most 32 * 2^8 = 2^13.  The
+  // result is the same either way, since numerator and normaliser share the
+  // reference; the common tile pays no max reduction.
   auto softmax = [&](const f32x16& s0, const f32x16& s1, bf16x8* pf) {
-    // row max over the 32 scores of this lane (a tree of 3-input max), then
-    // across the lane pair l, l^32 that shares the row
-    float t3[11];
+    // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block
+    // t/2.  The sum covers the bf16 weights the MFMA multiplies (dot2 with 1,1).
+    auto weights = [&]() {
+      const float mc = (m == -INFINITY) ? 0.f : m * scale;
+      f32x16 p0, p1;
 #pragma unroll
-    for (int r = 0; r < 5; ++r) t3[r] = fmaxf(s0[3 * r], fmaxf(s0[3 * r + 1], s0[3 * r + 2]));
+      for (int r = 0; r < 16; ++r) {
+        p0[r] = fast_exp2(fmaf(s0[r], scale, -mc));
+        p1[r] = fast_exp2(fmaf(s1[r], scale, -mc));
+      }
+      pf[0] = __builtin_convertvector(p0.lo, bf16x8);
+      pf[1] = __builtin_convertvector(p0.hi, bf16x8);
+      pf[2] = __builtin_convertvector(p1.lo, bf16x8);
+      pf[3] = __builtin_convertvector(p1.hi, bf16x8);
+      float t = 0.f;
 #pragma unroll
-    for (int r = 0; r < 5; ++r) t3[5 + r] = fmaxf(s1[3 * r], fmaxf(s1[3 * r + 1], s1[3 * r + 2]));
-    t3[10] = fmaxf(s0[15], s1[15]);
-    float mx = fmaxf(fmaxf(fmaxf(t3[0], t3[1]), fmaxf(t3[2], t3[3])),
-                     fmaxf(fmaxf(t3[4], t3[5]), fmaxf(t3[6], t3[7])));
-    mx = fmaxf(mx, fmaxf(t3[8], fmaxf(t3[9], t3[10])));
-    {
-      const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
-                                                       false, false);
-      mx = fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));
+      for (int f = 0; f < 4; ++f) {
+        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 0, 1), ones2, t, false);
+        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 2, 3), ones2, t, false);
+        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 4, 5), ones2, t, false);
+        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 6, 7), ones2, t, false);
+      }
+      return t;
+    };
+    float t = INFINITY;
+    if (!__any(m == -INFINITY)) t = weights();
+    if (__any(!(t <= 8192.f))) {
+      // row max over the 32 scores of this lane (a tree of 3-input max), then
+      // across the lane pair l, l^32 that shares the row
+      float t3[11];
+#pragma unroll
+      for (int r = 0; r < 5; ++r) t3[r] = fmaxf(s0[3 * r], fmaxf(s0[3 * r + 1], s0[3 * r + 2]));
+#pragma unroll
+      for (int r = 0; r < 5; ++r) t3[5 + r] = fmaxf(s1[3 * r], fmaxf(s1[3 * r + 1], s1[3 * r + 2]));
+      t3[10] = fmaxf(s0[15], s1[15]);
+      float mx = fmaxf(fmaxf(fmaxf(t3[0], t3[1]), fmaxf(t3[2], t3[3])),
+                       fmaxf(fmaxf(t3[4], t3[5]), fmaxf(t3[6], t3[7])));
+      mx = fmaxf(mx, fmaxf(t3[8], fmaxf(t3[9], t3[10])));
+      {
+        const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                         false, false);
+        mx = fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));
+      }
+      const bool grow = (mx - m) * scale > 8.f;
+      if (__any(grow)) {
+        const float m_new = fmaxf(m, mx);
+        const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2((m - m_new) * scale);
+        m = m_new;
+        l *= alpha;
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+      }
+      t = weights();
     }
-    // The reference max m only moves when a score exceeds it by more than
-    // 2^8 after exponentiation; otherwise P may reach 256 (harmless in fp32
-    // and bf16) and the rescale of O and l is skipped.  The result is the
-    // same: numerator and normaliser share the reference.
-    const bool grow = (mx - m) * scale > 8.f;
-    if (__any(grow)) {
-      const float m_new = fmaxf(m, mx);
-      const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2((m - m_new) * scale);
-      m = m_new;
-      l *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
-    }
-    const float mc = (m == -INFINITY) ? 0.f : m * scale;
-    f32x16 p0, p1;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      p0[r] = fast_exp2(fmaf(s0[r], scale, -mc));
-      p1[r] = fast_exp2(fmaf(s1[r], scale, -mc));
-    }
-    // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block t/2.
-    // The normaliser sums the bf16 weights the MFMA multiplies (dot2 with 1,1).
-    pf[0] = __builtin_convertvector(p0.lo, bf16x8);
-    pf[1] = __builtin_convertvector(p0.hi, bf16x8);
-    pf[2] = __builtin_convertvector(p1.lo, bf16x8);
-    pf[3] = __builtin_convertvector(p1.hi, bf16x8);
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 0, 1), ones2, l, false);
-      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 2, 3), ones2, l, false);
-      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 4, 5), ones2, l, false);
-      l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[t], pf[t], 6, 7), ones2, l, false);
-    }
+    l += t;
   };
 
   // O^T += V^T P^T for one tile.
