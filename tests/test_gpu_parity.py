@@ -106,6 +106,31 @@ def test_needles_pin_window_sink_and_anchor_boundaries():
     assert_parity(de, oracle.attention(qb, kb, vb, None, mode=oracle.MODE_DENSE), "dense, needles")
 
 
+@pytest.mark.parametrize("n_sink", [4, 0])
+def test_logits_rising_along_the_keys_move_the_reference_max(n_sink):
+    """Logits that climb by 15-60 log2 units per key tile (up to ~1200 over the sequence): the
+    weights would overflow fp32 unless the kernels move their reference max, tile after tile.
+    Heads whose logits fall along the keys keep the first reference."""
+    L, Hq, Hkv, d, w, gamma = 1200, 4, 1, 128, 700, 16
+    q, k, v, cu = make((L,), Hq, Hkv, d, seed=13, std=0.5)
+    g = torch.Generator().manual_seed(14)
+    u = torch.randn(d, generator=g)
+    u /= u.norm()
+    ramp = torch.linspace(0.0, 96.0, L)          # key j sits at ramp[j] along u
+    k = (0.1 * k.float() + ramp[:, None, None] * u).to(torch.bfloat16)
+    gain = torch.tensor([1.0, -1.0, 0.5, 2.0])   # per query head: rising, falling, slower, faster
+    q = (0.1 * q.float() + 48.0 * gain[None, :, None] * u).to(torch.bfloat16)
+    sp, de, dl = run_all(q, k, v, cu, w, n_sink, gamma)
+    for x in (sp, de, dl):
+        assert torch.isfinite(x.float()).all()
+    qb, kb, vb = (to_oracle_bits(x) for x in (q, k, v))
+    ref, ref_sp, _ = oracle.delta_attention(qb, kb, vb, None, window=w, n_sink=n_sink, gamma=gamma,
+                                            return_parts=True)
+    assert_parity(sp, ref_sp, "sparse kernel, rising logits")
+    assert_parity(dl, ref, "delta path, rising logits")
+    assert_parity(de, oracle.attention(qb, kb, vb, None, mode=oracle.MODE_DENSE), "dense, rising logits")
+
+
 def test_covered_groups_equal_sparse_output_bitwise_and_runs_are_deterministic():
     L, Hq, Hkv, d, w, s, gamma = 4096, 8, 2, 128, 512, 64, 64
     q, k, v, cu = make((L,), Hq, Hkv, d, seed=11)
