@@ -49,12 +49,27 @@ def errors(got: np.ndarray, ref: np.ndarray) -> dict:
             "nan": int(np.isnan(got).sum())}
 
 
-def assert_parity(got, ref, what="", max_abs=MAX_ABS, mean_abs=MEAN_ABS):
+def bf16_half_ulp(x: np.ndarray) -> np.ndarray:
+    """Half the spacing of bf16 values (8 significant bits) at |x|: the most one
+    round-to-nearest to bf16 can move a value of that magnitude."""
+    a = np.abs(np.asarray(x, dtype=np.float64))
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a > 0, np.exp2(e - 8), 0.0)
+
+
+def assert_parity(got, ref, what="", max_abs=MAX_ABS, mean_abs=MEAN_ABS, slack=None):
+    """max-abs and mean-abs against the oracle; `slack` (elementwise, optional) is
+    an extra rounding the computation is documented to make, forgiven in the
+    max-abs check only."""
     if isinstance(got, torch.Tensor):
         got = got.float().cpu().numpy().astype(np.float64)
     err = errors(got, ref)
     assert err["nan"] == 0, f"{what}: NaN in output {err}"
-    assert err["max_abs"] <= max_abs and err["mean_abs"] <= mean_abs, f"{what}: {err}"
+    worst = err["max_abs"]
+    if slack is not None:
+        worst = float(np.max(np.maximum(np.abs(got - ref) - slack, 0.0)))
+        err["max_abs_beyond_slack"] = worst
+    assert worst <= max_abs and err["mean_abs"] <= mean_abs, f"{what}: {err}"
     return err
 
 

@@ -1,0 +1,89 @@
+"""Seeded random configurations against the fp64 oracle, over whole tensors.
+
+Each case draws a batch and the method's parameters at random: one to three
+sequences of 1..2000 tokens (equal lengths through the fixed-length call,
+otherwise ragged through cu_seqlens), 1 or 2 kv heads with GQA ratios 1..8,
+d = 64 or 128, windows from 1 key to past the longest sequence, 0..300 sinks
+and gamma from 1 to past the longest sequence.  The sparse, dense and Delta
+calls run through the C ABI, the Delta call in every schedule that applies
+(default, unfused, and fused when supported), and every output element is
+compared with the oracle.  Tolerances as elsewhere: max-abs 2e-2, mean-abs
+2e-3; the unfused schedule's second rounding (the sparse row is stored in
+bf16 before Delta is added) is forgiven in the max-abs check, up to half a
+bf16 ulp of the sparse value.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from sampling import assert_parity, bf16_half_ulp, to_oracle_bits
+
+pytestmark = pytest.mark.gpu
+
+
+def draw(seed):
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 4))
+    if rng.random() < 0.3:
+        seqlens = (int(rng.integers(1, 1200)),) * B
+    else:
+        seqlens = tuple(int(x) for x in rng.integers(1, 2000, B))
+    Hkv = int(rng.choice([1, 2]))
+    G = int(rng.choice([1, 2, 3, 4, 8]))
+    d = int(rng.choice([64, 128]))
+    Lmax = max(seqlens)
+    window = int(rng.choice([1, int(rng.integers(1, 600)), int(rng.integers(1, 600)),
+                             Lmax + int(rng.integers(0, 50))]))
+    n_sink = int(rng.choice([0, int(rng.integers(0, 8)), int(rng.integers(0, 8)),
+                             int(rng.integers(0, 300))]))
+    gamma = int(rng.choice([1, 2, int(rng.integers(3, 130)), int(rng.integers(3, 130)), 64,
+                            Lmax + 1]))
+    return seqlens, Hkv * G, Hkv, d, window, n_sink, gamma
+
+
+SEEDS = list(range(100, 132))
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_random_configuration_matches_oracle(seed):
+    from paper_2505_11254_amd import binding as lib
+    from paper_2505_11254_amd.inputs import random_qkv
+    seqlens, Hq, Hkv, d, w, s, gamma = draw(seed)
+    print(f"seed {seed}: seqlens={seqlens} Hq={Hq} Hkv={Hkv} d={d} window={w} n_sink={s} "
+          f"gamma={gamma}", flush=True)
+    q, k, v, cu = random_qkv(seqlens, Hq, Hkv, d, seed=seed)
+    qd, kd, vd, cud = (x.cuda() for x in (q, k, v, cu))
+    fixed = len(set(seqlens)) == 1
+    N = max(seqlens)
+    kw = dict(B=len(seqlens)) if fixed else dict(cu_seqlens=cud, max_seqlen=N)
+    sp = lib.sparse_attn_prefill(qd, kd, vd, window=w, n_sink=s, **kw)
+    de = lib.dense_causal_attn_prefill(qd, kd, vd, **kw)
+    runs = {"default": lib.delta_attn_prefill(qd, kd, vd, window=w, n_sink=s, gamma=gamma, **kw)}
+    schedules = [("unfused", lib.STEP_ALL)]
+    if lib.fused_supported(Hq, Hkv, gamma):
+        schedules.append(("fused", lib.STEP_ALL | lib.STEP_FUSED))
+    for name, steps in schedules:
+        out = torch.full_like(qd, float("nan"))
+        ws = torch.full((lib.workspace_bytes(len(seqlens), N, Hq, Hkv, d, gamma) // 4,),
+                        float("nan"), device=qd.device)
+        lib.delta_attn_prefill_steps(qd, kd, vd, out, ws, steps, window=w, n_sink=s, gamma=gamma,
+                                     B=len(seqlens), cu_seqlens=None if fixed else cud,
+                                     max_seqlen=N)
+        runs[name] = out
+    torch.cuda.synchronize()
+    bits = [to_oracle_bits(x) for x in (q, k, v)]
+    cun = cu.numpy().astype(np.int64)
+    ref, ref_sp, _ = oracle.delta_attention(*bits, cun, window=w, n_sink=s, gamma=gamma,
+                                            return_parts=True)
+    assert_parity(sp, ref_sp, f"seed {seed} sparse")
+    assert_parity(de, oracle.attention(*bits, cun, mode=oracle.MODE_DENSE), f"seed {seed} dense")
+    for name, out in runs.items():
+        # the unfused schedule stores the sparse row in bf16 before adding Delta: a
+        # second rounding, up to half a bf16 ulp of the sparse value, which matters
+        # where outputs are O(1) (one-key windows) rather than wide averages
+        slack = bf16_half_ulp(ref_sp) if name == "unfused" or (
+            name == "default" and not lib.fused_supported(Hq, Hkv, gamma)) else None
+        assert_parity(out, ref, f"seed {seed} delta ({name})", slack=slack)
