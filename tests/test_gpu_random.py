@@ -10,7 +10,8 @@ calls run through the C ABI, the Delta call in every schedule that applies
 compared with the oracle.  Tolerances as elsewhere: max-abs 2e-2, mean-abs
 2e-3; the unfused schedule's second rounding (the sparse row is stored in
 bf16 before Delta is added) is forgiven in the max-abs check, up to half a
-bf16 ulp of the sparse value.
+bf16 ulp of the sparse value.  A second test draws key-block-list
+configurations the same way (top-k, vertical-slash and Star layouts).
 """
 from __future__ import annotations
 
@@ -87,3 +88,72 @@ def test_random_configuration_matches_oracle(seed):
         slack = bf16_half_ulp(ref_sp) if name == "unfused" or (
             name == "default" and not lib.fused_supported(Hq, Hkv, gamma)) else None
         assert_parity(out, ref, f"seed {seed} delta ({name})", slack=slack)
+
+
+def draw_lists(seed):
+    """A random block-list configuration: batch, heads, query block size, gamma and
+    a list layout with random parameters."""
+    from paper_2505_11254_amd import blocklists as BL
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 4))
+    seqlens = tuple(int(x) for x in rng.integers(1, 2000, B))
+    Hkv = int(rng.choice([1, 2]))
+    G = int(rng.choice([1, 2, 4, 8]))
+    d = int(rng.choice([64, 128]))
+    # the list mode needs each workgroup's rows of a head (256 / h of them, h the
+    # heads of a GQA group sharing a workgroup) inside one query block
+    h = 1
+    while h * 2 <= 8 and G % (h * 2) == 0:
+        h *= 2
+    block_q = int(rng.choice([bq for bq in (64, 128, 256) if bq >= 256 // h]))
+    gamma = int(rng.choice([1, 2, int(rng.integers(3, 130)), 64, max(seqlens) + 1]))
+    kind = int(rng.integers(0, 3))
+    if kind == 0:
+        bl = BL.block_topk(seqlens, Hkv, block_q, k=int(rng.integers(1, 12)), seed=seed)
+    elif kind == 1:
+        bl = BL.vertical_slash(seqlens, Hkv, block_q, n_vertical=int(rng.integers(0, 6)),
+                               n_local=int(rng.integers(0, 6)),
+                               slash_offsets=tuple(int(x) for x in rng.integers(1, 40, 2)),
+                               seed=seed)
+    else:
+        bl = BL.star(seqlens, Hkv, block_q, anchor=64 * int(rng.integers(1, 8)),
+                     context=block_q * int(rng.integers(1, 4)))
+    return seqlens, Hkv * G, Hkv, d, block_q, gamma, bl
+
+
+LIST_SEEDS = list(range(200, 216))
+
+
+@pytest.mark.parametrize("seed", LIST_SEEDS)
+def test_random_block_lists_match_oracle(seed):
+    from paper_2505_11254_amd import binding as lib
+    from paper_2505_11254_amd.inputs import random_qkv
+    seqlens, Hq, Hkv, d, block_q, gamma, bl = draw_lists(seed)
+    print(f"seed {seed}: seqlens={seqlens} Hq={Hq} Hkv={Hkv} d={d} block_q={block_q} "
+          f"gamma={gamma} nnz={bl.idx.size}", flush=True)
+    q, k, v, cu = random_qkv(seqlens, Hq, Hkv, d, seed=seed)
+    qd, kd, vd, cud = (x.cuda() for x in (q, k, v, cu))
+    ptr, idx = bl.to("cuda")
+    N = max(seqlens)
+    kw = dict(cu_seqlens=cud, max_seqlen=N)
+    lkw = dict(block_q=block_q, block_ptr=ptr, block_idx=idx)
+    sp = lib.blocksparse_attn_prefill(qd, kd, vd, **lkw, **kw)
+    fused_ok = lib.fused_supported_blocksparse(Hq, Hkv, gamma, block_q)
+    runs = {}
+    for name, steps in [("default", 0), ("unfused", lib.STEP_ALL)] + (
+            [("fused", lib.STEP_ALL | lib.STEP_FUSED)] if fused_ok else []):
+        out = torch.full_like(qd, float("nan"))
+        ws = torch.full((lib.workspace_bytes(len(seqlens), N, Hq, Hkv, d, gamma) // 4,),
+                        float("nan"), device=qd.device)
+        runs[name] = lib.delta_attn_prefill_blocksparse(qd, kd, vd, gamma=gamma, out=out,
+                                                         workspace=ws, steps=steps, **lkw, **kw)
+    torch.cuda.synchronize()
+    bits = [to_oracle_bits(x) for x in (q, k, v)]
+    ref, ref_sp, _ = oracle.block_delta_attention(*bits, cu.numpy().astype(np.int64),
+                                                  blk_ptr=bl.ptr, blk_idx=bl.idx,
+                                                  block_q=block_q, gamma=gamma, return_parts=True)
+    assert_parity(sp, ref_sp, f"seed {seed} sparse (lists)")
+    for name, out in runs.items():
+        slack = bf16_half_ulp(ref_sp) if name == "unfused" or (
+            name == "default" and not fused_ok) else None
+        assert_parity(out, ref, f"seed {seed} delta over lists ({name})", slack=slack)
