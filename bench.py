@@ -52,15 +52,15 @@ def pair_counts(seqlens, window, n_sink, gamma):
     return sp, dr, dc
 
 
-def epilogue_bytes(wl):
+def epilogue_bytes(wl, cover):
     """Algorithmic HBM bytes of the Delta correction: for every group whose
-    anchor is not covered by the sparse key set, read and write the gamma-1
-    corrected bf16 rows, write the bf16 anchor row, read its fp32 sparse and
-    dense rows; dense tail rows are written once."""
+    anchor is not covered by the sparse key set (anchors a >= cover), read and
+    write the gamma-1 corrected bf16 rows, write the bf16 anchor row, read its
+    fp32 sparse and dense rows; dense tail rows are written once."""
     tot = 0
     for L in wl.seqlens:
         nA = L // wl.gamma
-        first_open = -(-(wl.n_sink + wl.window) // wl.gamma)  # first anchor index with Delta
+        first_open = -(-cover // wl.gamma)  # first anchor index with Delta
         n_open = max(0, nA - first_open)
         per_group = (wl.gamma - 1) * wl.d * 2 * 2 + wl.d * 2 + 2 * wl.d * 4
         tot += n_open * per_group * wl.Hq + (L - nA * wl.gamma) * wl.d * 2 * wl.Hq
@@ -80,14 +80,14 @@ def plan_chunk(wl):
     return -(-(-(-L // nC)) // 64) * 64
 
 
-def merge_bytes(wl):
+def merge_bytes(wl, cover):
     """Algorithmic HBM bytes of the fused schedule's merge: for every dense row
-    it merges (anchors whose Delta is not zero, and tail rows), read the fp32
-    partial (d values, max, normaliser) of each key chunk the row reaches and
-    write the merged fp32 row."""
+    it merges (anchors a >= cover, whose Delta is not zero, and tail rows), read
+    the fp32 partial (d values, max, normaliser) of each key chunk the row
+    reaches and write the merged fp32 row."""
     chunk = plan_chunk(wl)
     tot = 0
-    first_open = -(-(wl.n_sink + wl.window) // wl.gamma)
+    first_open = -(-cover // wl.gamma)
     for L in wl.seqlens:
         nA = L // wl.gamma
         rows = [i * wl.gamma for i in range(first_open, nA)] + list(range(nA * wl.gamma, L))
@@ -426,20 +426,25 @@ def main():
 
     # the unfused schedule on the same inputs (sparse kernel, strided rows, then
     # the in-place Delta pass over the output), for comparison
-    unfused_ms = None
+    unfused_ms, unfused_k = None, None
     if fused and not args.path_only:
-        run_u = lambda: run_steps(binding.STEP_ALL)
-        run_u()
-        u0 = torch.cuda.Event(enable_timing=True)
-        u1 = torch.cuda.Event(enable_timing=True)
+        order_u = [(SP, binding.STEP_SPARSE), ("strided_dense_rows", binding.STEP_DENSE_ROWS),
+                   ("delta_epilogue", binding.STEP_CORRECT)]
+        run_steps(binding.STEP_ALL)
+        ev_u = [[torch.cuda.Event(enable_timing=True) for _ in range(len(order_u) + 1)]
+                for _ in range(args.steps)]
         torch.cuda.synchronize()
-        u0.record(stream)
-        for _ in range(args.steps):
-            run_u()
-        u1.record(stream)
+        for s_ in range(args.steps):
+            for i, (_, bits) in enumerate(order_u):
+                ev_u[s_][i].record(stream)
+                run_steps(bits)
+            ev_u[s_][len(order_u)].record(stream)
         torch.cuda.synchronize()
-        unfused_ms = u0.elapsed_time(u1) / args.steps
-        log(f"unfused schedule: {unfused_ms:.3f} ms/step")
+        unfused_k = {name: sum(e[i].elapsed_time(e[i + 1]) for e in ev_u) / args.steps
+                     for i, (name, _) in enumerate(order_u)}
+        unfused_ms = sum(unfused_k.values())
+        log(f"unfused schedule: {unfused_ms:.3f} ms/step; "
+            + ", ".join(f"{n} {t:.3f} ms" for n, t in unfused_k.items()))
 
     # sparse attention alone (f*, StreamingLLM) on the same inputs: the cost
     # Delta adds on top of the sparse method it corrects
@@ -449,6 +454,25 @@ def main():
                                           run=sparse_run)
         log(f"sparse only: {sparse_only_ms:.3f} ms; "
             f"delta overhead x{ms_per_step / sparse_only_ms:.3f}")
+
+    # what a plain device-to-device copy reaches on this GPU (1 GiB read + 1 GiB
+    # written), the practical ceiling of the HBM-bound kernels
+    copy_gbs = None
+    if not args.path_only:
+        src = torch.empty(1 << 29, dtype=torch.int16, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        c0.record(stream)
+        for _ in range(5):
+            dst.copy_(src)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        copy_gbs = 2 * src.numel() * 2 * 5 / c0.elapsed_time(c1) / 1e6
+        log(f"device copy: {copy_gbs:.0f} GB/s")
+        del src, dst
 
     T = wl.total_tokens
     _, dr_pairs, dc_pairs = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
@@ -484,10 +508,20 @@ def main():
                                "useful_tflops": flops["dense_rows"] / k_ms["strided_dense_rows"]
                                / 1e9},
     }
-    hbm_kernel, hbm_bytes = (("dense_row_merge", merge_bytes(wl)) if fused
-                             else ("delta_epilogue", epilogue_bytes(wl)))
+    # anchors below `cover` keep their sparse rows (sink + window covers [0, a]);
+    # no anchor is covered under key-block lists
+    cover = wl.n_sink + wl.window if args.basis == "streaming" else 0
+    hbm_kernel, hbm_bytes = (("dense_row_merge", merge_bytes(wl, cover)) if fused
+                             else ("delta_epilogue", epilogue_bytes(wl, cover)))
     per_kernel[hbm_kernel] = {"ms": k_ms[hbm_kernel], "gbs": hbm_bytes / k_ms[hbm_kernel] / 1e6,
                               "hbm_frac": hbm_bytes / k_ms[hbm_kernel] / 1e6 / PEAK_HBM_GBS}
+    # the unfused schedule's Delta pass over the output (when it was timed)
+    unfused_epi = None
+    if unfused_k:
+        eb = epilogue_bytes(wl, cover)
+        unfused_epi = {"ms": round(unfused_k["delta_epilogue"], 4),
+                       "gbs": round(eb / unfused_k["delta_epilogue"] / 1e6, 1),
+                       "hbm_frac": round(eb / unfused_k["delta_epilogue"] / 1e6 / PEAK_HBM_GBS, 4)}
     if dense_ms is not None:
         per_kernel["dense_causal"] = {"ms": dense_ms,
                                       "useful_tflops": flops["dense_causal"] / dense_ms / 1e9}
@@ -522,6 +556,8 @@ def main():
         "config": dict(wl.describe(), parallelism="single_gpu", **basis_cfg),
         "schedule": "fused" if fused else "unfused",
         "unfused_ms_per_step": round(unfused_ms, 4) if unfused_ms else None,
+        "unfused_delta_epilogue": unfused_epi,
+        "device_copy_gbs": round(copy_gbs, 1) if copy_gbs else None,
         "speedup_vs_dense_causal": round(dense_ms / ms_per_step, 2) if dense_ms else None,
         "sparse_only_ms": round(sparse_only_ms, 4) if sparse_only_ms else None,
         "delta_overhead_vs_sparse": (round(ms_per_step / sparse_only_ms, 4) if sparse_only_ms

@@ -691,17 +691,22 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
     const int hh = idx / DC, dc = idx % DC;
     const int h = h0 + hh;
     const int64_t slot0 = (((int64_t)b * a.Hq + h) * a.nR_max + r) * a.nC;
-    float M = -INFINITY;
-    for (int cc = 0; cc < nc; ++cc) M = fmaxf(M, a.part_ml[(slot0 + cc) * 2]);
-    float lsum = 0.f;
+    // one pass with a running max M (the loads of every chunk are independent,
+    // so they can all be in flight together): chunks with no visible key
+    // (max -inf) are skipped, and acc, lsum move to a larger M by 2^(M - Mn)
+    float M = -INFINITY, lsum = 0.f;
     f32x8 acc = f32x8{};
+#pragma unroll 4
     for (int cc = 0; cc < nc; ++cc) {
       const float mc = a.part_ml[(slot0 + cc) * 2];
-      if (mc == -INFINITY) continue;
-      const float w = fast_exp2(mc - M);
-      lsum += w * a.part_ml[(slot0 + cc) * 2 + 1];
+      const float lc = a.part_ml[(slot0 + cc) * 2 + 1];
       const f32x8 po = *(const f32x8*)(a.part_o + (slot0 + cc) * D + dc * 8);
-      acc += w * po;
+      if (mc == -INFINITY) continue;
+      const float Mn = fmaxf(M, mc);
+      const float sc = fast_exp2(M - Mn), w = fast_exp2(mc - Mn);
+      lsum = lsum * sc + w * lc;
+      acc = acc * sc + w * po;
+      M = Mn;
     }
     const f32x8 dense = acc * (1.f / lsum);
     if (EPI == kEpiMergeDense) {
@@ -722,17 +727,33 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
   if (!anchor || EPI != kEpiDelta) return;
   __syncthreads();
 
-  // rows pos+1 .. pos+gamma-1 for heads [h0, h1): nh*D contiguous values per row
+  // rows pos+1 .. pos+gamma-1 for heads [h0, h1): nh*D contiguous values per
+  // row.  Each thread loads kU vectors before it stores any, so that many
+  // reads per thread are in flight (a load and a store of one address per
+  // iteration would leave one).
+  constexpr int kU = 4;
   const int per_row = nh * DC;
   const int64_t total = (int64_t)(a.gamma - 1) * per_row;
-  for (int64_t u = tid; u < total; u += kEpiThreads) {
-    const int i = (int)(u / per_row);
-    const int rem = (int)(u % per_row);
-    const int hh = rem / DC, dc = rem % DC;
-    uint16_t* p = a.out + ((sq.base + pos + 1 + i) * a.Hq + h0 + hh) * (int64_t)D + dc * 8;
-    const bf16x8_t x = *(const bf16x8_t*)p;
-    const f32x8 y = __builtin_convertvector(x, f32x8) + *(const f32x8*)(delta + hh * D + dc * 8);
-    *(bf16x8_t*)p = __builtin_convertvector(y, bf16x8_t);
+  for (int64_t u0 = tid; u0 < total; u0 += (int64_t)kU * kEpiThreads) {
+    uint16_t* p[kU];
+    bf16x8_t x[kU];
+    int dl[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t u = min(u0 + (int64_t)j * kEpiThreads, total - 1);
+      const int i = (int)(u / per_row);
+      const int rem = (int)(u % per_row);
+      const int hh = rem / DC, dc = rem % DC;
+      p[j] = a.out + ((sq.base + pos + 1 + i) * a.Hq + h0 + hh) * (int64_t)D + dc * 8;
+      dl[j] = hh * D + dc * 8;
+      x[j] = *(const bf16x8_t*)p[j];
+    }
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      if (u0 + (int64_t)j * kEpiThreads >= total) break;
+      const f32x8 y = __builtin_convertvector(x[j], f32x8) + *(const f32x8*)(delta + dl[j]);
+      *(bf16x8_t*)p[j] = __builtin_convertvector(y, bf16x8_t);
+    }
   }
 }
 
