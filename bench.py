@@ -52,6 +52,84 @@ def pair_counts(seqlens, window, n_sink, gamma):
     return sp, dr, dc
 
 
+def heads_per_block(G):
+    """Query heads sharing an attention workgroup: the largest power of two
+    dividing G, at most 8 (one wavefront of 32 rows per head and sub-tile)."""
+    h = 1
+    while h * 2 <= 8 and G % (h * 2) == 0:
+        h *= 2
+    return h
+
+
+def fused_heads_per_block(G, gamma):
+    h = heads_per_block(G)
+    while h >= 1:
+        if G % h == 0 and (32 * (8 // h)) % gamma == 0:
+            return h
+        h //= 2
+    return 0
+
+
+def executed_pairs(wl, kind, hpw=None):
+    """Per head: (row, key) pairs the MFMAs execute, whole tiles counted, as the
+    kernels tile the work.  A workgroup holds hpw heads x (8 / hpw) wavefronts
+    of 32 rows; a wavefront runs every 64-key tile of its workgroup's range
+    in which some key is visible to some of its rows and skips the others.
+    kind: "sparse" (sink + window rows), "dense_rows" (anchors and tail rows,
+    key axis split in chunks) or "dense" (every row, causal)."""
+    import numpy as np
+    G = wl.Hq // wl.Hkv
+    hpw = hpw or heads_per_block(G)
+    ppw = 8 // hpw
+    chunk = plan_chunk(wl)
+    tot = 0
+    for L in wl.seqlens:
+        nA = L // wl.gamma
+        Lc = nA * wl.gamma
+        if kind == "dense_rows":
+            n_rows = nA + (L - Lc)
+            r = np.arange(n_rows, dtype=np.int64)
+            pos = np.where(r < nA, r * wl.gamma, Lc + (r - nA))
+        else:
+            n_rows = L
+            pos = np.arange(L, dtype=np.int64)
+        if n_rows == 0:
+            continue
+        nw = -(-n_rows // 32)
+        w = np.arange(nw, dtype=np.int64)
+        R0 = (w // ppw) * 32 * ppw
+        R1 = np.minimum(R0 + 32 * ppw, n_rows)
+        wlo = pos[32 * w]
+        whi = pos[np.minimum(32 * w + 31, n_rows - 1)]
+        blo, bhi = pos[R0], pos[R1 - 1]
+        if kind == "dense":
+            tot += int((whi // 64 + 1).sum()) * 64 * 32
+        elif kind == "dense_rows":
+            nC = -(-L // chunk) if L else 0
+            for c in range(nC):
+                kc0 = c * chunk
+                t_a = kc0 // 64
+                t_b = (np.minimum(kc0 + chunk, bhi + 1) + 63) // 64
+                live = kc0 <= bhi
+                n = np.clip(np.minimum(t_b, whi // 64 + 1) - t_a, 0, None)
+                tot += int(np.where(live, n, 0).sum()) * 64 * 32
+        else:
+            s_, win = wl.n_sink, wl.window
+            ta1 = (np.minimum(s_, bhi + 1) + 63) // 64
+            tb0 = np.maximum(np.maximum(0, blo - win + 1) // 64, ta1)
+            tb1 = np.maximum(tb0, bhi // 64 + 1)
+            n_sink_t = np.minimum(ta1, whi // 64 + 1)
+            # window tiles [tb0, tb1) the wavefront does not skip: a key at or
+            # below its last row, and not wholly before every row's window
+            # (unless a sink tile)
+            t = tb0[:, None] + np.arange(int((tb1 - tb0).max()) if nw else 0)[None, :]
+            k0, k1 = 64 * t, 64 * t + 63
+            run = (t < tb1[:, None]) & (k0 <= whi[:, None]) & \
+                ~((k0 >= s_) & (wlo[:, None] - k1 >= win))
+            tot += int((n_sink_t.sum() + run.sum())) * 64 * 32
+    return tot
+
+
 def epilogue_bytes(wl, cover):
     """Algorithmic HBM bytes of the Delta correction: for every group whose
     anchor is not covered by the sparse key set (anchors a >= cover), read and
@@ -207,6 +285,48 @@ BASES = {
 }
 
 
+def other_workload(binding, generate, wl, dev, steps, with_dense):
+    """The metric is quoted at 131K as well as 1M: the whole Delta path
+    (delta_attn_prefill) on another workload, with the dense causal baseline,
+    timed with HIP events on the launch stream."""
+    import torch
+    q, k, v, cu = generate(wl, device=dev)
+    kw = dict(B=wl.B) if wl.fixed_length else dict(cu_seqlens=cu, max_seqlen=wl.max_seqlen)
+    out = torch.empty_like(q)
+    ws = torch.empty(binding.workspace_bytes(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma),
+                     dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    run = lambda: binding.delta_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink,
+                                            gamma=wl.gamma, out=out, workspace=ws, **kw)
+    n, t0 = 0, time.perf_counter()
+    while n < 2 or time.perf_counter() - t0 < 0.5:
+        run()
+        torch.cuda.synchronize()
+        n += 1
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    rec = {"ms_per_step": round(ms, 4), "tokens_per_s": round(wl.total_tokens / (ms / 1e3), 1),
+           "steps": steps, "warmup": n, "dense_causal_ms": None, "speedup_vs_dense_causal": None}
+    if with_dense:
+        binding.dense_causal_attn_prefill(q, k, v, out=out, **kw)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        binding.dense_causal_attn_prefill(q, k, v, out=out, **kw)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dms = e0.elapsed_time(e1)
+        rec["dense_causal_ms"] = round(dms, 3)
+        rec["speedup_vs_dense_causal"] = round(dms / ms, 2)
+    log(f"{wl.name}: delta path {ms:.3f} ms/step ({rec['tokens_per_s']:.0f} tokens/s), "
+        f"dense causal {rec['dense_causal_ms']} ms")
+    return rec
+
+
 def gamma_sweep(args, wl, binding, q, k, v, kw, dev):
     """Delta path vs sparse-only time for several gammas (same inputs)."""
     import dataclasses
@@ -301,6 +421,9 @@ def main():
                     help="time only the Delta path (and the dense baseline unless --no-dense): "
                          "skip the unfused-schedule and sparse-only comparison runs, so a "
                          "profiled run holds the path's own launches")
+    ap.add_argument("--no-131k", action="store_true",
+                    help="skip the second workload the metric is quoted on (the 131K layer), "
+                         "timed after the headline one")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB device buffer, a dispatch of known traffic "
                          "against which HBM byte counters are scaled")
@@ -479,6 +602,14 @@ def main():
     sp_pairs = sparse_pairs
     fl = lambda pairs: 4.0 * wl.d * wl.Hq * pairs
     flops = {"sparse": fl(sp_pairs), "dense_rows": fl(dr_pairs), "dense_causal": fl(dc_pairs)}
+    # executed flops: whole tiles the MFMAs run, as the kernels tile the work
+    # (sink + window basis only; key-block lists are counted as useful flops)
+    G = wl.Hq // wl.Hkv
+    xflops = {"dense_rows": fl(executed_pairs(wl, "dense_rows")),
+              "dense_causal": fl(executed_pairs(wl, "dense"))}
+    if args.basis == "streaming":
+        xflops["sparse"] = fl(executed_pairs(
+            wl, "sparse", fused_heads_per_block(G, wl.gamma) if fused else heads_per_block(G)))
 
     # dense causal baseline (the in-house quadratic kernel)
     dense_ms = None
@@ -502,12 +633,14 @@ def main():
             f"TFLOP/s useful)")
         del out_d
 
-    per_kernel = {
-        SP: {"ms": k_ms[SP], "useful_tflops": flops["sparse"] / k_ms[SP] / 1e9},
-        "strided_dense_rows": {"ms": k_ms["strided_dense_rows"],
-                               "useful_tflops": flops["dense_rows"] / k_ms["strided_dense_rows"]
-                               / 1e9},
-    }
+    def rates(key, ms):
+        r = {"ms": ms, "useful_tflops": flops[key] / ms / 1e9}
+        if key in xflops:
+            r["executed_tflops"] = xflops[key] / ms / 1e9
+        return r
+
+    per_kernel = {SP: rates("sparse", k_ms[SP]),
+                  "strided_dense_rows": rates("dense_rows", k_ms["strided_dense_rows"])}
     # anchors below `cover` keep their sparse rows (sink + window covers [0, a]);
     # no anchor is covered under key-block lists
     cover = wl.n_sink + wl.window if args.basis == "streaming" else 0
@@ -523,14 +656,16 @@ def main():
                        "gbs": round(eb / unfused_k["delta_epilogue"] / 1e6, 1),
                        "hbm_frac": round(eb / unfused_k["delta_epilogue"] / 1e6 / PEAK_HBM_GBS, 4)}
     if dense_ms is not None:
-        per_kernel["dense_causal"] = {"ms": dense_ms,
-                                      "useful_tflops": flops["dense_causal"] / dense_ms / 1e9}
+        per_kernel["dense_causal"] = rates("dense_causal", dense_ms)
+    # MFMA utilisation of the dominant kernel: executed flops (whole tiles run)
+    # over its event time, beside the useful (element-exact) rate
     dom = max((SP, "strided_dense_rows"), key=lambda n: per_kernel[n]["ms"])
-    dom_flops = flops["sparse"] if dom == SP else flops["dense_rows"]
-    achieved = dom_flops / per_kernel[dom]["ms"] / 1e9
+    achieved = per_kernel[dom].get("executed_tflops", per_kernel[dom]["useful_tflops"])
     roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "flops": "executed" if "executed_tflops" in per_kernel[dom] else "useful",
+                "useful_achieved": round(per_kernel[dom]["useful_tflops"], 2),
                 "traffic": load_traffic(dom, wl.name)}
 
     cpu = None
@@ -538,6 +673,19 @@ def main():
         log("timing the oracle on a bounded sample of the workload ...")
         cpu = cpu_baseline(wl, q, k, v)
         log(f"cpu baseline: {cpu}")
+
+    # the 131K layer, the other size the metric is quoted at (after the
+    # headline workload's tensors are released)
+    also = None
+    if (wl.name == HEADLINE and args.basis == "streaming" and not args.path_only
+            and not args.no_131k):
+        del q, k, v, out
+        if "ws" in locals():
+            del ws
+        torch.cuda.empty_cache()
+        also = {"llama8b_layer_131k": other_workload(binding, generate,
+                                                      WORKLOADS["llama8b_layer_131k"], dev,
+                                                      max(args.steps, 20), not args.no_dense)}
 
     value = T / (ms_per_step / 1e3)
     rec = {
@@ -566,6 +714,7 @@ def main():
         "kernels": {n: {kk: round(vv, 4) for kk, vv in d_.items()} for n, d_ in per_kernel.items()},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "also": also,
     }
     print(json.dumps(rec), flush=True)
 
