@@ -68,6 +68,7 @@ CASES = [
     ((600,), 8, 2, 128, 64, 64, "full"),                    # every tile: dense attention
     ((600,), 8, 2, 64, 64, 16, "empty"),                    # own query block only
     ((1100,), 4, 1, 128, 256, 48, "vertical_slash"),        # gamma fits no slab: unfused
+    ((0, 700, 0, 90), 8, 2, 128, 64, 32, "topk"),           # empty sequences in the batch
 ]
 
 

@@ -29,6 +29,7 @@ CASES = [
     ((3000,), 4, 1, 128, 256, 16, 256),           # gamma 256: one head per block
     ((500,), 2, 1, 64, 16, 2, 2),                 # gamma 2, d 64: the largest LDS exchange
     ((700,), 1, 1, 128, 50, 3, 2),                # gamma 2, d 128: the largest LDS exchange
+    ((0, 450, 0, 64), 8, 2, 128, 64, 8, 32),      # empty sequences inside a ragged batch
 ]
 
 

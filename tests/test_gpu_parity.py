@@ -62,6 +62,8 @@ SMALL = [
     ((2500,), 6, 3, 128, 200, 300, 48),           # GQA 2, sinks wider than the window
     ((130, 70), 2, 1, 128, 33, 1, 7),             # odd gamma, short sequences
     ((300,), 4, 1, 128, 2 ** 31 - 1, 0, 16),      # the largest window: sparse = dense
+    ((0, 300, 0, 77, 0), 8, 2, 128, 64, 8, 16),   # empty sequences: leading, inner, trailing
+    ((0, 0, 129), 4, 4, 64, 32, 4, 64),           # only the last sequence has tokens, d 64
 ]
 
 

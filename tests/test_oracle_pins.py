@@ -214,6 +214,18 @@ def test_varlen_equals_separate_sequences():
         assert np.array_equal(packed[s0:s1], alone)
 
 
+def test_empty_sequences_change_nothing():
+    """A ragged batch may hold sequences of length zero (repeated offsets): they own no rows
+    and leave every other sequence's result as it is without them."""
+    seqlens = (0, 70, 0, 33, 0)
+    (q, k, v), _, cu = rand_problem(seqlens, 4, 2, 16, seed=13)
+    assert list(cu) == [0, 0, 70, 70, 103, 103]
+    packed = oracle.delta_attention(q, k, v, cu, window=6, n_sink=2, gamma=8)
+    dense = np.array([0, 70, 103])
+    assert np.array_equal(packed, oracle.delta_attention(q, k, v, dense, window=6, n_sink=2,
+                                                         gamma=8))
+
+
 def test_row_entry_point_equals_full_algorithm():
     seqlens = (100, 37)
     (q, k, v), _, cu = rand_problem(seqlens, 4, 2, 16, seed=12, bf16=True)
