@@ -108,14 +108,25 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 
-// 16 bytes per lane from a buffer into LDS at lds + 16*lane (LDS DMA).  The
-// builtin exists only for the GPU target; in the host pass of the kernel
-// templates it would silently drop the kernels' host stubs, so the host pass
-// sees an empty body.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint16_t* lds, int voff) {
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// 16 bytes per lane from a buffer into LDS at byte address lds + 16*lane (LDS
+// DMA; rsrc and lds are wave-uniform).  Written as asm so that the compiler
+// does not track the transfer: its wait-count pass would otherwise wait for
+// every DMA in flight before any LDS read it cannot prove disjoint from the
+// DMA's target (the V^T reads of the current tile, while the next tile's DMA
+// is in flight).  The main loop waits for each tile's DMA itself (vmcnt)
+// before the barrier that publishes the tile.  The host pass of the kernel
+// templates sees an empty body.
+__device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t lds, int voff) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16,
-                                           voff, 0, 0, 0);
+  // the descriptor and M0 must be scalar registers: read them from the first
+  // lane so the compiler cannot hand the asm a vector copy
+  const i32x4 sr = {__builtin_amdgcn_readfirstlane(rsrc[0]), __builtin_amdgcn_readfirstlane(rsrc[1]),
+                    __builtin_amdgcn_readfirstlane(rsrc[2]), __builtin_amdgcn_readfirstlane(rsrc[3])};
+  const int m0v = __builtin_amdgcn_readfirstlane((int)lds);
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :: "v"(voff), "s"(sr), "{m0}"(m0v) : "memory");
 #endif
 }
 
@@ -256,6 +267,11 @@ void attn_kernel(Args a) {
     // iteration and must not wait behind the prefetch loads issued in it
     __builtin_amdgcn_s_waitcnt(0x0F70);
   }
+  // Queries pre-scaled by log2(e)/sqrt(d) and rounded to bf16 once, so the
+  // score accumulators hold base-2 logits and the weights need no multiply.
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk)
+    qf[kk] = __builtin_convertvector(__builtin_convertvector(qf[kk], f32x8) * a.scale_log2, bf16x8);
 
   const int64_t kv_stride = (int64_t)a.Hkv * D;  // elements between consecutive keys
   const uint16_t* kbase = a.k + (sq.base * a.Hkv + g) * (int64_t)D;
@@ -279,22 +295,34 @@ void attn_kernel(Args a) {
     dma_koff[i] = (int)(r * kv_stride * 2) + (pc ^ LD::kswz(r)) * 16;
     dma_voff[i] = (int)(r * kv_stride * 2) + (pc ^ LD::vswz(r)) * 16;
   }
+  // Buffer descriptors (stride 0, raw buffer): base at the tile's first key,
+  // num_records up to the sequence end, at most one tile.  Everything here is
+  // wave-uniform (scalar registers).
+  const uint32_t key_bytes = (uint32_t)__builtin_amdgcn_readfirstlane((int)(kv_stride * 2));
+  const uint32_t tile_bytes = key_bytes * kKeyTile;
+  const uint64_t kaddr0 = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uintptr_t)kbase) |
+                          (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)((uintptr_t)kbase >> 32)) << 32;
+  const uint64_t vaddr0 = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uintptr_t)vbase) |
+                          (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)((uintptr_t)vbase >> 32)) << 32;
+  const int L_s = __builtin_amdgcn_readfirstlane(L);
+  const uint32_t smem_lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)smem;
   auto dma = [&](int tile, int stage) {
     if (tile < 0) return;  // a list entry the key set ignores
-    const int64_t key0 = (int64_t)tile * kKeyTile;
-    const int64_t bytes = (L - key0) * kv_stride * 2;
-    const int nrec = (int)max((int64_t)0, min(bytes, (int64_t)0x7fffffff));
-    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(kbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
-    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(vbase + key0 * kv_stride), (short)0, nrec, 0x00020000);
-    uint16_t* ks = smem + stage * LD::stageElems;
-    uint16_t* vs = ks + LD::kElems;
+    const uint32_t tu = (uint32_t)__builtin_amdgcn_readfirstlane(tile);
+    const uint64_t off = (uint64_t)tu * tile_bytes;
+    int keys = L_s - (int)(tu * kKeyTile);
+    keys = keys < 0 ? 0 : keys;
+    keys = keys > kKeyTile ? kKeyTile : keys;
+    const uint32_t nrec = (uint32_t)keys * key_bytes;
+    const uint64_t ka = kaddr0 + off, va = vaddr0 + off;
+    const i32x4 kr = {(int)(uint32_t)ka, (int)((uint32_t)(ka >> 32) & 0xffffu), (int)nrec, 0x00020000};
+    const i32x4 vr = {(int)(uint32_t)va, (int)((uint32_t)(va >> 32) & 0xffffu), (int)nrec, 0x00020000};
+    const uint32_t st0 = smem_lds + (uint32_t)(stage * LD::stageElems) * 2;
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
-      const int region = (wave_s * RPW + i) * 512;  // in bf16 elements
-      dma16(kr, ks + region, dma_koff[i]);
-      dma16(vr, vs + region, dma_voff[i]);
+      const uint32_t region = (uint32_t)((wave_s * RPW + i) * 512) * 2;  // bytes
+      dma16(kr, st0 + region, dma_koff[i]);
+      dma16(vr, st0 + (uint32_t)LD::kElems * 2 + region, dma_voff[i]);
     }
   };
 
@@ -341,9 +369,13 @@ void attn_kernel(Args a) {
   f32x16 o[D / 32];
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
-  float m = -INFINITY;  // reference max of raw scores (same in lanes l and l^32)
+  // Reference `ref` of the base-2 logits (same in lanes l and l^32; has_ref: a
+  // reference exists) and -ref in every register of nref, the block the
+  // score accumulators start from, so they hold logit - ref.
+  float ref = 0.f;
+  bool has_ref = false;
+  f32x16 nref = f32x16{};
   float l = 0.f;        // this lane's share of the softmax normaliser
-  const float scale = a.scale_log2;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
@@ -351,8 +383,8 @@ void attn_kernel(Args a) {
   // key 8*(r/4) + 4*h + r%4 in s0, that key + 32 in s1); keys outside a row's
   // key set read -inf when `masked`.
   auto qk = [&](const uint16_t* ks, int tile, bool masked, f32x16& s0, f32x16& s1) {
-    s0 = f32x16{};
-    s1 = f32x16{};
+    s0 = nref;
+    s1 = nref;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       const bf16x8 ka = *(const bf16x8*)(ks + kread[kk]);
@@ -395,54 +427,66 @@ void attn_kernel(Args a) {
     }
   };
 
-  // Online-softmax update with one tile's scores: adds the tile's weights to
-  // l and returns them as bf16 P^T fragments, moving the reference max first
-  // when it has to.
+  // Online-softmax update with one tile's scores s = logit - ref: adds the
+  // tile's weights to l and returns them as bf16 P^T fragments, moving the
+  // reference first when it has to.
   //
-  // The reference max m lags the true running max: weights are taken against
-  // the current m, and only if some lane's share of the tile's weight sum
-  // exceeds 2^13 (or no reference exists yet) does the wave take the row max
-  // of the tile.  m then moves to it when a score exceeds m by more than 2^8
-  // after exponentiation (rescaling O and l), and the weights are taken
-  // again.  Every weight stays below 2^13 (harmless in fp32 and bf16): a lane
-  // whose scores all lie within 2^8 of m sums at most 32 * 2^8 = 2^13.  The
-  // result is the same either way, since numerator and normaliser share the
-  // reference; the common tile pays no max reduction.
-  auto softmax = [&](const f32x16& s0, const f32x16& s1, bf16x8* pf) {
+  // The reference lags the true running max: weights are taken against the
+  // current one, and only if some lane's share of the tile's weight sum exceeds
+  // 2^13 (or some lane has no reference yet) does the wave take the row max
+  // of the tile.  ref then moves up by it when a score exceeds ref by more than 8
+  // (a weight above 2^8), rescaling O and l, and the weights are taken again.
+  // Every weight stays below 2^13 (harmless in fp32 and bf16): a lane whose
+  // scores all lie within 8 of ref sums at most 32 * 2^8 = 2^13.  The result is
+  // the same either way, since numerator and normaliser share the reference;
+  // the common tile pays no max reduction and no subtraction.
+  auto softmax = [&](f32x16& s0, f32x16& s1, bf16x8* pf) {
     // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block
-    // t/2.  The sum covers the bf16 weights the MFMA multiplies (dot2 with 1,1).
+    // t/2.  The sum covers the bf16 weights the MFMA multiplies (dot2 with 1,1),
+    // in two chains.
     auto weights = [&]() {
-      const float mc = (m == -INFINITY) ? 0.f : m * scale;
       f32x16 p0, p1;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p0[r] = fast_exp2(fmaf(s0[r], scale, -mc));
-        p1[r] = fast_exp2(fmaf(s1[r], scale, -mc));
+      for (int i = 0; i < 16; ++i) {
+        p0[i] = fast_exp2(s0[i]);
+        p1[i] = fast_exp2(s1[i]);
       }
       pf[0] = __builtin_convertvector(p0.lo, bf16x8);
       pf[1] = __builtin_convertvector(p0.hi, bf16x8);
       pf[2] = __builtin_convertvector(p1.lo, bf16x8);
       pf[3] = __builtin_convertvector(p1.hi, bf16x8);
-      float t = 0.f;
+      float ta = 0.f, tb = 0.f;
 #pragma unroll
       for (int f = 0; f < 4; ++f) {
-        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 0, 1), ones2, t, false);
-        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 2, 3), ones2, t, false);
-        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 4, 5), ones2, t, false);
-        t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 6, 7), ones2, t, false);
+        ta = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 0, 1), ones2, ta, false);
+        tb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 2, 3), ones2, tb, false);
+        ta = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 4, 5), ones2, ta, false);
+        tb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 6, 7), ones2, tb, false);
       }
-      return t;
+      if (MODE != kSparse) {
+        // the exponentials go two at a time with two other VALU instructions
+        // (conversions, sums) between them: a wave issues one exponential
+        // every ~15 clocks and fits its other VALU work into those gaps
+        __builtin_amdgcn_sched_group_barrier(0x400, 4, 0);
+#pragma unroll
+        for (int i = 0; i < 14; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+      }
+      return ta + tb;
     };
     float t = INFINITY;
-    if (!__any(m == -INFINITY)) t = weights();
+    if (!__any(!has_ref)) t = weights();
     if (__any(!(t <= 8192.f))) {
       // row max over the 32 scores of this lane (a tree of 3-input max), then
       // across the lane pair l, l^32 that shares the row
       float t3[11];
 #pragma unroll
-      for (int r = 0; r < 5; ++r) t3[r] = fmaxf(s0[3 * r], fmaxf(s0[3 * r + 1], s0[3 * r + 2]));
+      for (int i = 0; i < 5; ++i) t3[i] = fmaxf(s0[3 * i], fmaxf(s0[3 * i + 1], s0[3 * i + 2]));
 #pragma unroll
-      for (int r = 0; r < 5; ++r) t3[5 + r] = fmaxf(s1[3 * r], fmaxf(s1[3 * r + 1], s1[3 * r + 2]));
+      for (int i = 0; i < 5; ++i) t3[5 + i] = fmaxf(s1[3 * i], fmaxf(s1[3 * i + 1], s1[3 * i + 2]));
       t3[10] = fmaxf(s0[15], s1[15]);
       float mx = fmaxf(fmaxf(fmaxf(t3[0], t3[1]), fmaxf(t3[2], t3[3])),
                        fmaxf(fmaxf(t3[4], t3[5]), fmaxf(t3[6], t3[7])));
@@ -452,14 +496,24 @@ void attn_kernel(Args a) {
                                                          false, false);
         mx = fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));
       }
-      const bool grow = (mx - m) * scale > 8.f;
+      // a lane without a reference takes its tile max (if it sees any key);
+      // one with a reference moves only up
+      const bool seen = mx != -INFINITY;
+      const bool grow = has_ref ? mx > 8.f : seen;
       if (__any(grow)) {
-        const float m_new = fmaxf(m, mx);
-        const float alpha = (m_new == -INFINITY) ? 1.f : fast_exp2((m - m_new) * scale);
-        m = m_new;
+        const float dm = has_ref ? fmaxf(mx, 0.f) : (seen ? mx : 0.f);
+        const float alpha = has_ref ? fast_exp2(-dm) : 0.f;  // l and O are still zero without one
+        ref += dm;
+        has_ref = has_ref || seen;
         l *= alpha;
 #pragma unroll
         for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          s0[i] -= dm;
+          s1[i] -= dm;
+          nref[i] = -ref;
+        }
       }
       t = weights();
     }
@@ -628,7 +682,7 @@ void attn_kernel(Args a) {
       }
     }
     if (half == 0) {
-      a.part_ml[slot * 2] = m * scale;  // -inf when no key of the chunk is visible
+      a.part_ml[slot * 2] = has_ref ? ref : -INFINITY;  // -inf when no key of the chunk is visible
       a.part_ml[slot * 2 + 1] = lt;
     }
   }
