@@ -18,6 +18,7 @@ Everything else goes to stderr.
 from __future__ import annotations
 
 import argparse
+import re
 import hashlib
 import json
 import os
@@ -397,6 +398,76 @@ def correction_sweep(args, wl, binding, q, k, v, kw, dev):
         del ws
 
 
+class PowerSampler:
+    """Board power and shader clock, sampled once a second by `amd-smi metric
+    -p -c` in a child process.  It is started before this process touches the
+    GPU (a process that has initialised the GPU starts no other program) and
+    stopped by its own PID; without amd-smi every reading is None."""
+
+    def __init__(self, seconds=900):
+        import shutil
+        import subprocess
+        import tempfile
+        self.proc, self.path = None, None
+        exe = shutil.which("amd-smi")
+        if exe is None:
+            return
+        fd, self.path = tempfile.mkstemp(prefix="bench_smi_", suffix=".csv")
+        self.out = os.fdopen(fd, "w")
+        try:
+            self.proc = subprocess.Popen([exe, "metric", "-p", "-c", "--csv", "-w", "1", "-W",
+                                          str(int(seconds))], stdout=self.out,
+                                         stderr=subprocess.DEVNULL, stdin=subprocess.DEVNULL,
+                                         env=dict(os.environ, PYTHONUNBUFFERED="1"))
+        except OSError:
+            self.proc = None
+
+    def stop(self):
+        if self.proc is not None and self.proc.poll() is None:
+            self.proc.terminate()
+            try:
+                self.proc.wait(timeout=10)
+            except Exception:
+                self.proc.kill()
+                self.proc.wait(timeout=10)
+        if self.path is not None:
+            self.out.close()
+
+    def summary(self, t0, t1):
+        """median socket power (W) and mean-over-XCDs gfx clock (MHz) of the
+        samples whose whole-second timestamp lies in [t0, t1] (epoch seconds)"""
+        if self.path is None or not os.path.exists(self.path):
+            return None
+        rows, header = [], None
+        for line in open(self.path):
+            f = line.strip().split(",")
+            if f and f[0] == "timestamp":
+                header = f
+                continue
+            if header is None or len(f) != len(header) or not f[0].isdigit():
+                continue
+            r = dict(zip(header, f))
+            if not (int(t0) <= int(r["timestamp"]) <= int(t1)):
+                continue
+            try:
+                clks = [float(v) for k, v in r.items()
+                        if re.fullmatch(r"gfx_\d+_clk", k) and v.replace(".", "", 1).isdigit()]
+                rows.append((float(r["socket_power"]), sum(clks) / len(clks)))
+            except (KeyError, ValueError, ZeroDivisionError):
+                continue
+        if not rows:
+            return None
+        med = lambda xs: sorted(xs)[len(xs) // 2]
+        return {"socket_power_w": med([r[0] for r in rows]), "gfx_clk_mhz": round(med([r[1] for r in rows]), 1),
+                "samples": len(rows),
+                "source": "amd-smi metric -p -c, 1 s samples over the warmup and timed steps"}
+
+    def close(self):
+        self.stop()
+        if self.path is not None and os.path.exists(self.path):
+            os.unlink(self.path)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -427,6 +498,8 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB device buffer, a dispatch of known traffic "
                          "against which HBM byte counters are scaled")
+    ap.add_argument("--no-power", action="store_true",
+                    help="do not sample board power and shader clock with amd-smi")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -435,6 +508,16 @@ def main():
               "run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
+    # started before anything initialises the GPU
+    sampler = None if args.no_power else PowerSampler()
+    try:
+        run_main(args, sampler)
+    finally:
+        if sampler is not None:
+            sampler.close()
+
+
+def run_main(args, sampler):
     import torch
 
     from paper_2505_11254_amd import HEADLINE, WORKLOADS, binding
@@ -515,6 +598,7 @@ def main():
         if evs is not None:
             evs[len(order)].record(stream)
 
+    t_pow0 = time.time()
     if args.warmup is not None:
         for _ in range(args.warmup):
             step()
@@ -539,6 +623,7 @@ def main():
     end.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
+    t_pow1 = time.time()
     ms_total = start.elapsed_time(end)
     ms_per_step = ms_total / args.steps
     k_ms = {name: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps
@@ -715,6 +800,9 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "also": also,
+        # board power and shader clock while the headline steps ran: the
+        # strided kernel holds the board at its power limit, below 2.4 GHz
+        "device": sampler.summary(t_pow0, t_pow1) if sampler is not None else None,
     }
     print(json.dumps(rec), flush=True)
 
