@@ -463,18 +463,16 @@ void attn_kernel(Args a) {
         ta = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 4, 5), ones2, ta, false);
         tb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 6, 7), ones2, tb, false);
       }
-      if (MODE != kSparse) {
-        // the exponentials go two at a time with two other VALU instructions
-        // (conversions, sums) between them: a wave issues one exponential
-        // every ~15 clocks and fits its other VALU work into those gaps
-        __builtin_amdgcn_sched_group_barrier(0x400, 4, 0);
+      // the exponentials go two at a time with two other VALU instructions
+      // (conversions, sums) between them: a wave issues one exponential
+      // every ~15 clocks and fits its other VALU work into those gaps
+      __builtin_amdgcn_sched_group_barrier(0x400, 4, 0);
 #pragma unroll
-        for (int i = 0; i < 14; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+      for (int i = 0; i < 14; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
+      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
       return ta + tb;
     };
     float t = INFINITY;
