@@ -215,3 +215,70 @@ def test_planted_block_mistake_fails_brute_force(name, tmp_path):
         ref = brute_block_parts(q, k, v, cu, bl.ptr, bl.idx, block_q, 16)[0]
         failed |= not np.allclose(got, ref, rtol=0, atol=1e-11)
     assert failed, f"mutant {name} passed"
+
+
+# ---- the row entry point of sparse attention under block lists ----
+
+BROW_SEQLENS = (300, 0, 129, 1)
+
+
+def _block_row_pins_pass(orc) -> bool:
+    """block_attention(rows=R) equals the whole-tensor call at R bit for bit,
+    and the brute-force block-mask softmax, on a ragged GQA batch."""
+    (q, k, v), (qf, kf, vf), cu = rand_problem(BROW_SEQLENS, 4, 2, 16, seed=21, bf16=True)
+    bl = random_lists(BROW_SEQLENS, 2, 64, seed=22)
+    sparse = brute_block_parts(qf, kf, vf, cu, bl.ptr, bl.idx, 64, 1)[2]
+    rng = np.random.default_rng(23)
+    rows = [(b, h, i) for b, L in enumerate(BROW_SEQLENS) if L for h in range(4)
+            for i in {0, L - 1, min(L - 1, 64), min(L - 1, 63)}]
+    rows += [(b, int(rng.integers(0, 4)), int(rng.integers(0, L)))
+             for b, L in enumerate(BROW_SEQLENS) if L for _ in range(L // 4)]
+    rows = [rows[n] for n in rng.permutation(len(rows))]
+    try:
+        kw = dict(blk_ptr=bl.ptr, blk_idx=bl.idx, block_q=64)
+        full = orc.block_attention(q, k, v, cu, **kw)
+        got = orc.block_attention(q, k, v, cu, rows=rows, **kw)
+    except RuntimeError:
+        return False
+    for n, (b, h, i) in enumerate(rows):
+        t = cu[b] + i
+        if not np.array_equal(got[n], full[t, h]):
+            return False
+        if not np.allclose(got[n], sparse[t, h], rtol=0, atol=1e-12):
+            return False
+    return True
+
+
+def test_block_attention_rows_equal_whole_tensor_and_brute_force():
+    assert _block_row_pins_pass(oracle.Oracle())
+
+
+@pytest.mark.parametrize("bad", [(4, 0, 0), (0, 4, 0), (0, 0, 300), (1, 0, 0), (-1, 0, 0)])
+def test_block_attention_rows_out_of_range_are_rejected(bad):
+    (q, k, v), _, cu = rand_problem(BROW_SEQLENS, 4, 2, 16, seed=24, bf16=True)
+    bl = random_lists(BROW_SEQLENS, 2, 64, seed=22)
+    with pytest.raises(RuntimeError):
+        oracle.block_attention(q, k, v, cu, blk_ptr=bl.ptr, blk_idx=bl.idx, block_q=64,
+                               rows=[(0, 0, 0), bad])
+
+
+BLOCK_ROW_MUTANTS = {
+    "block_row_head_and_position_swapped": (
+        "        h = (int)rows[3 * it + 1];\n        i = rows[3 * it + 2];\n      } else {",
+        "        h = (int)rows[3 * it + 2];\n        i = rows[3 * it + 1];\n      } else {"),
+    "block_row_sequence_taken_as_head": (
+        "        b = (int)rows[3 * it];\n        h = (int)rows[3 * it + 1];\n        i = rows[3 * it + 2];\n      } else {",
+        "        b = (int)rows[3 * it + 1];\n        h = (int)rows[3 * it];\n        i = rows[3 * it + 2];\n      } else {"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BLOCK_ROW_MUTANTS))
+def test_planted_block_row_decode_mistake_fails(name, tmp_path):
+    src = os.path.join(os.path.dirname(oracle.__file__), "delta_oracle.c")
+    text = open(src).read()
+    old, new = BLOCK_ROW_MUTANTS[name]
+    assert text.count(old) == 1, name
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(text.replace(old, new))
+    orc = oracle.Oracle(oracle.build(force=True, src=str(mutated), dst=str(tmp_path / "m.so")))
+    assert not _block_row_pins_pass(orc), f"mutant {name} passed"

@@ -421,3 +421,105 @@ def test_planted_variant_mistake_fails_matrix_form(name, tmp_path):
         ref = brute_variant(q, k, v, cu, 12, 2, 8, mode, params)
         failed |= not np.allclose(got, ref, rtol=0, atol=1e-11)
     assert failed, f"mutant {name} passed"
+
+
+# ---- the row entry points of plain attention (f and f*), used as checkers at large sizes ----
+#
+# A row needs only its own key set (Eq. 1; Sec. 3 for f*), so the oracle can be
+# evaluated on any list of (sequence, head, row) triples.  These pins hold that
+# list form to the whole-tensor form bit for bit, and both to the brute-force
+# masked-softmax matrices, on a ragged GQA batch with empty sequences.
+
+ROW_SEQLENS = (57, 0, 90, 1, 33)
+ROW_SHAPE = dict(Hq=4, Hkv=2, d=16)
+ROW_W, ROW_S = 7, 2
+
+
+def _row_triples(seqlens, Hq, seed):
+    """Every head of the first, last and window-edge rows of each sequence, plus
+    random triples, shuffled, with repeats."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for b, L in enumerate(seqlens):
+        for i in {0, L - 1, min(L - 1, ROW_W), min(L - 1, ROW_W + ROW_S)} if L else ():
+            rows += [(b, h, i) for h in range(Hq)]
+        rows += [(b, int(rng.integers(0, Hq)), int(rng.integers(0, L))) for _ in range(L // 3)] if L else []
+    rows += rows[:5]
+    order = rng.permutation(len(rows))
+    return [rows[n] for n in order]
+
+
+def _row_pins_pass(orc: oracle.Oracle) -> bool:
+    """attention(rows=R) equals the whole-tensor call at R (outputs, score max
+    and normaliser) and brute force, for f and f*."""
+    (q, k, v), (qf, kf, vf), cu = rand_problem(ROW_SEQLENS, seed=41, bf16=True, **ROW_SHAPE)
+    _, dense, sparse = brute_parts(qf, kf, vf, cu, ROW_W, ROW_S, 1)
+    rows = _row_triples(ROW_SEQLENS, ROW_SHAPE["Hq"], seed=42)
+    try:
+        for mode, ref in ((oracle.MODE_DENSE, dense), (oracle.MODE_SPARSE, sparse)):
+            full, m, z = orc.attention(q, k, v, cu, mode=mode, window=ROW_W, n_sink=ROW_S,
+                                       return_stats=True)
+            got, gm, gz = orc.attention(q, k, v, cu, mode=mode, window=ROW_W, n_sink=ROW_S,
+                                        rows=rows, return_stats=True)
+            for n, (b, h, i) in enumerate(rows):
+                t = cu[b] + i
+                if not (np.array_equal(got[n], full[t, h]) and gm[n] == m[t, h]
+                        and gz[n] == z[t, h]):
+                    return False
+                if not np.allclose(got[n], ref[t, h], rtol=0, atol=1e-12):
+                    return False
+    except RuntimeError:
+        return False
+    return True
+
+
+def test_attention_rows_equal_whole_tensor_and_brute_force():
+    assert _row_pins_pass(oracle.Oracle())
+
+
+def test_attention_whole_tensor_matches_brute_force():
+    (q, k, v), (qf, kf, vf), cu = rand_problem(ROW_SEQLENS, seed=43, bf16=True, **ROW_SHAPE)
+    _, dense, sparse = brute_parts(qf, kf, vf, cu, ROW_W, ROW_S, 1)
+    for mode, ref in ((oracle.MODE_DENSE, dense), (oracle.MODE_SPARSE, sparse)):
+        got = oracle.attention(q, k, v, cu, mode=mode, window=ROW_W, n_sink=ROW_S)
+        np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("bad", [(5, 0, 0), (-1, 0, 0), (0, 4, 0), (0, -1, 0), (0, 0, 57),
+                                 (1, 0, 0), (3, 0, 1), (0, 0, -1)])
+def test_attention_rows_out_of_range_are_rejected(bad):
+    """Triples outside the batch (sequence, head, or row past its sequence,
+    including any row of an empty sequence) are an argument error."""
+    (q, k, v), _, cu = rand_problem(ROW_SEQLENS, seed=44, bf16=True, **ROW_SHAPE)
+    for mode in (oracle.MODE_DENSE, oracle.MODE_SPARSE):
+        with pytest.raises(RuntimeError):
+            oracle.attention(q, k, v, cu, mode=mode, window=ROW_W, n_sink=ROW_S,
+                             rows=[(0, 0, 0), bad])
+
+
+ROW_MUTANTS = {
+    "row_head_and_position_swapped": (
+        "        h = (int)rows[3 * it + 1];\n        i = rows[3 * it + 2];\n        o = out + it * d;",
+        "        h = (int)rows[3 * it + 2];\n        i = rows[3 * it + 1];\n        o = out + it * d;"),
+    "row_sequence_taken_as_head": (
+        "        b = (int)rows[3 * it];\n        h = (int)rows[3 * it + 1];\n        i = rows[3 * it + 2];\n        o = out + it * d;",
+        "        b = (int)rows[3 * it + 1];\n        h = (int)rows[3 * it];\n        i = rows[3 * it + 2];\n        o = out + it * d;"),
+    "row_stats_offset_by_one": (
+        "        mo = m_out ? m_out + it : NULL;\n        zo = z_out ? z_out + it : NULL;\n      } else {",
+        "        mo = m_out ? m_out + (it + 1) % n_rows : NULL;\n        zo = z_out ? z_out + it : NULL;\n      } else {"),
+    "row_position_global_not_local": (
+        "        i = rows[3 * it + 2];\n        o = out + it * d;",
+        "        i = rows[3 * it + 2] - cu[rows[3 * it]];\n        o = out + it * d;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ROW_MUTANTS))
+def test_planted_row_decode_mistake_fails_the_row_pins(name, tmp_path):
+    src = os.path.join(os.path.dirname(oracle.__file__), "delta_oracle.c")
+    text = open(src).read()
+    old, new = ROW_MUTANTS[name]
+    assert text.count(old) == 1, f"mutation site for {name} not found exactly once"
+    mutated = tmp_path / "mutant.c"
+    mutated.write_text(text.replace(old, new))
+    lib = oracle.build(force=True, src=str(mutated), dst=str(tmp_path / "libmutant.so"))
+    assert not _row_pins_pass(oracle.Oracle(lib)), f"mutant {name} passed the row pins"
