@@ -398,27 +398,45 @@ def correction_sweep(args, wl, binding, q, k, v, kw, dev):
         del ws
 
 
+def profiler_loaded(env=None) -> bool:
+    """True when a profiler's tool library is loaded into this process (rocprofv3
+    and rocprofiler-sdk set ROCPROF*/ROCP_* variables, HSA_TOOLS_LIB, or preload
+    their libraries).  Such a library initialises the GPU in every process that
+    inherits it, so this process then starts no other program."""
+    env = os.environ if env is None else env
+    for key in env:
+        if key.startswith(("ROCPROF", "ROCP_")) or key == "HSA_TOOLS_LIB":
+            return True
+    return "rocprofiler" in env.get("LD_PRELOAD", "") or "roctracer" in env.get("LD_PRELOAD", "")
+
+
 class PowerSampler:
     """Board power and shader clock, sampled once a second by `amd-smi metric
-    -p -c` in a child process.  It is started before this process touches the
-    GPU (a process that has initialised the GPU starts no other program) and
-    stopped by its own PID; without amd-smi every reading is None."""
+    -p -c` in a child process (the amd-smi script run by this interpreter, so
+    the child does not exec another program).  It is started before this
+    process touches the GPU, and never under a profiler (`profiler_loaded`):
+    there the profiler's preloaded library has already initialised the GPU in
+    this process and would do so again in the child before it runs.  Stopped
+    by its own PID; without amd-smi, or under a profiler, every reading is
+    None."""
 
-    def __init__(self, seconds=900):
+    def __init__(self, seconds=900, env=None):
         import shutil
         import subprocess
         import tempfile
         self.proc, self.path = None, None
+        env = dict(os.environ if env is None else env)
+        self.declined = profiler_loaded(env)
         exe = shutil.which("amd-smi")
-        if exe is None:
+        if exe is None or self.declined:
             return
         fd, self.path = tempfile.mkstemp(prefix="bench_smi_", suffix=".csv")
         self.out = os.fdopen(fd, "w")
         try:
-            self.proc = subprocess.Popen([exe, "metric", "-p", "-c", "--csv", "-w", "1", "-W",
-                                          str(int(seconds))], stdout=self.out,
+            self.proc = subprocess.Popen([sys.executable, exe, "metric", "-p", "-c", "--csv", "-w",
+                                          "1", "-W", str(int(seconds))], stdout=self.out,
                                          stderr=subprocess.DEVNULL, stdin=subprocess.DEVNULL,
-                                         env=dict(os.environ, PYTHONUNBUFFERED="1"))
+                                         env=dict(env, PYTHONUNBUFFERED="1"))
         except OSError:
             self.proc = None
 

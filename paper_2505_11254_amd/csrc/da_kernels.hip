@@ -159,7 +159,9 @@ void attn_kernel(Args a) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // The sparse kernel classifies tiles per wave from wave-uniform bounds:
+  // with the wave index in a scalar register those tests stay scalar.
+  const int wave = MODE == kSparse ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
   const int half = lane >> 5;
   const int col = lane & 31;
 
@@ -224,8 +226,14 @@ void attn_kernel(Args a) {
     ta0 = (int)(kc0 / kKeyTile);
     ta1 = (int)((kc1 + kKeyTile - 1) / kKeyTile);
   }
-  const int n_a = ta1 - ta0;
-  const int n_iter = n_a + (tb1 - tb0);
+  // The tile range is block-uniform; the list loads above are vector loads,
+  // so say so explicitly, which keeps the loop counter and the per-tile tests
+  // in scalar registers.
+  ta0 = __builtin_amdgcn_readfirstlane(ta0);
+  tb0 = __builtin_amdgcn_readfirstlane(tb0);
+  lst0 = __builtin_amdgcn_readfirstlane(lst0);
+  const int n_a = __builtin_amdgcn_readfirstlane(ta1 - ta0);
+  const int n_iter = __builtin_amdgcn_readfirstlane(n_a + (tb1 - tb0));
 
   // ---- this wave's rows; lane (col) owns row wr0 + col
   const int wr0 = R0 + sub * kRowsPerWave;
@@ -346,7 +354,7 @@ void attn_kernel(Args a) {
   auto tile_at = [&](int it) -> int {
     if (it >= n_a) return tb0 + (it - n_a);
     if (MODE == kSparse && a.blk_ptr) {
-      const int e = a.blk_idx[lst0 + it];
+      const int e = __builtin_amdgcn_readfirstlane(a.blk_idx[lst0 + it]);
       return (e >= 0 && e < diag0) ? e : -1;
     }
     return ta0 + it;
@@ -582,10 +590,17 @@ void attn_kernel(Args a) {
       const int tile = tile_at(it);
       const int cls = classify(tile);
       const uint16_t* ks = smem + st * LD::stageElems;
-      if (cls == 1)
+      if (MODE == kSparse) {
+        // tile classes are scalar here: one copy of the tile body with the
+        // mask as a branch inside it, so the accumulators keep one register
+        // assignment across tiles (two copies made the compiler copy O
+        // between them at every step)
+        if (cls != 0) compute(ks, tile, cls == 2);
+      } else if (cls == 1) {
         compute(ks, tile, false);
-      else if (cls == 2)
+      } else if (cls == 2) {
         compute(ks, tile, true);
+      }
     }
   }
 

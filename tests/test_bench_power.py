@@ -35,3 +35,45 @@ def test_window_median_and_xcd_mean(tmp_path):
 def test_no_sample_in_window(tmp_path):
     text = HDR + "\n50,0,240,N/A,95,500,2400,95,500,2400,1900\n"
     assert sampler_on(tmp_path, text).summary(100, 110) is None
+
+
+def test_sampler_declines_under_a_profiler(monkeypatch):
+    """Under a profiler (whose preloaded tool library initialises the GPU in
+    every process that inherits it) no child program is started."""
+    import subprocess
+    started = []
+    monkeypatch.setattr(subprocess, "Popen", lambda *a, **k: started.append(a) or None)
+    for env in ({"ROCPROF_OUTPUT_PATH": "/tmp/x"}, {"ROCPROFILER_LIBRARY_CTOR": "1"},
+                {"ROCP_TOOL_LIBRARIES": "/opt/rocm/lib/x.so"}, {"HSA_TOOLS_LIB": "x.so"},
+                {"LD_PRELOAD": "/opt/rocm/lib/librocprofiler-sdk-tool.so"}):
+        assert bench.profiler_loaded(env)
+        s = bench.PowerSampler(env=env)
+        assert s.declined and s.proc is None and s.path is None
+        assert s.summary(0, 1) is None
+        s.close()
+    assert started == []
+    assert not bench.profiler_loaded({"PATH": "/usr/bin", "LD_PRELOAD": ""})
+
+
+def test_sampler_runs_amd_smi_with_this_interpreter(monkeypatch):
+    """Without a profiler the child is this interpreter running the amd-smi
+    script (no exec of another program through its #! line)."""
+    import shutil
+    import subprocess
+    calls = []
+
+    class P:
+        def __init__(self, argv, **kw):
+            calls.append((argv, kw))
+
+        def poll(self):
+            return 0
+
+    monkeypatch.setattr(shutil, "which", lambda name: "/opt/rocm/bin/amd-smi")
+    monkeypatch.setattr(subprocess, "Popen", P)
+    s = bench.PowerSampler(env={"PATH": "/usr/bin"})
+    assert not s.declined and len(calls) == 1
+    argv, kw = calls[0]
+    assert argv[0] == sys.executable and argv[1] == "/opt/rocm/bin/amd-smi"
+    assert not any(k.startswith("ROCP") for k in kw["env"])
+    s.close()
