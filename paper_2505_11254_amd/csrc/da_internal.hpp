@@ -21,6 +21,30 @@ constexpr int kAttnThreads = 64 * kAttnWaves;
 // Delta epilogue workgroups.
 constexpr int kEpiThreads = 256;
 
+// Division by a divisor fixed for a launch, for numerators below 2^31.  With
+// l = ceil(log2 d) and m = floor(2^(31+l) / d) + 1 < 2^32, floor(x / d) =
+// floor(x m / 2^(31+l)) for every 0 <= x < 2^31 (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", 1994, Thm. 4.2 with
+// N = 31).  A uniform numerator costs three scalar instructions instead of
+// a division routine.
+struct FastDiv {
+  uint32_t m;
+  uint32_t sh;  // 31 + l
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while (l < 32 && (1ull << l) < d) ++l;
+  FastDiv f;
+  f.m = (uint32_t)(((1ull << (31 + l)) / d) + 1);
+  f.sh = 31 + l;
+  return f;
+}
+
+__host__ __device__ __forceinline__ uint32_t fdiv(uint32_t x, FastDiv f) {
+  return (uint32_t)(((uint64_t)x * f.m) >> f.sh);
+}
+
 // Everything a kernel needs; passed by value as the kernel argument.
 struct Args {
   const uint16_t* q;  // [T, Hq, d] bf16
@@ -49,6 +73,9 @@ struct Args {
   int hpw, ppw;
   int n_hgroups;      // Hq / hpw
   int n_rtiles;       // row tiles (of 32 * ppw rows) per (sequence, head group)
+  // the launch's divisors: row tiles, key chunks, sequences, GQA group size
+  // Hq / Hkv, gamma, query block
+  FastDiv fd_rtiles, fd_nC, fd_B, fd_G, fd_gamma, fd_bq;
 
   // Workspace of the Delta path (nullptr for the plain attention calls).
   float* sa;          // [B][Hq][nA_max][d]      sparse output at anchor rows, fp32

@@ -39,6 +39,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 enum Mode { kSparse = 0, kDense = 1, kDenseRows = 2 };
+// Per-element masks of a partly visible key tile (tile classes 2..5).
+enum MaskKind { kMaskCausal = 2, kMaskWindow = 3, kMaskBoth = 4, kMaskAll = 5 };
 
 // LDS layout of one pipeline stage (bf16 elements): K and V tiles of 64 keys,
 // both row-major [key][dim] with unpadded rows of 2*D bytes.  Tiles arrive by
@@ -88,14 +90,14 @@ __device__ __forceinline__ Seq seq_of(const Args& a, int b) {
 //    uneven work (sequences of different lengths, triangular key ranges).
 //    Blocks past the last whole round of 8 chunks keep their index.
 constexpr int kXcdChunk = 64;
-__device__ __forceinline__ int64_t xcd_remap(int64_t i, int64_t n, bool contiguous) {
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t i, uint32_t n, bool contiguous) {
   if (contiguous) {
-    const int64_t per = n / 8;
+    const uint32_t per = n / 8;
     return i < per * 8 ? (i % 8) * per + i / 8 : i;
   }
-  const int64_t span = 8 * (int64_t)kXcdChunk;
+  const uint32_t span = 8 * kXcdChunk;
   if (i >= n / span * span) return i;
-  const int64_t k = i / 8;
+  const uint32_t k = i / 8;
   return ((i % 8) + 8 * (k / kXcdChunk)) * kXcdChunk + k % kXcdChunk;
 }
 
@@ -166,16 +168,19 @@ void attn_kernel(Args a) {
   const int col = lane & 31;
 
   // ---- which (sequence, head group, row tile[, key chunk]) this block owns
-  int64_t lid = xcd_remap(blockIdx.x, gridDim.x, a.n_hgroups % 8 == 0);
-  int rt = (int)(lid % a.n_rtiles);
-  lid /= a.n_rtiles;
+  // (grids hold fewer than 2^31 blocks; the divisors are the launch's)
+  uint32_t lid = xcd_remap(blockIdx.x, gridDim.x, a.n_hgroups % 8 == 0);
+  uint32_t q = fdiv(lid, a.fd_rtiles);
+  int rt = (int)(lid - q * (uint32_t)a.n_rtiles);
+  lid = q;
   int c = 0;
   if (MODE == kDenseRows) {
-    c = (int)(lid % a.nC);
-    lid /= a.nC;
+    q = fdiv(lid, a.fd_nC);
+    c = (int)(lid - q * (uint32_t)a.nC);
+    lid = q;
   }
-  const int b = (int)(lid % a.B);
-  const int hg = (int)(lid / a.B);
+  const int hg = (int)fdiv(lid, a.fd_B);
+  const int b = (int)(lid - (uint32_t)hg * (uint32_t)a.B);
   // Longest rows first: in the dense modes blocks dispatched together then have
   // (nearly) the same number of key tiles, start on the same tile and stay in
   // step, so they share each key/value tile in L2.
@@ -183,11 +188,12 @@ void attn_kernel(Args a) {
 
   const Seq sq = seq_of(a, b);
   const int L = sq.L;
-  const int G = a.Hq / a.Hkv;
-  const int h = hg * a.hpw + (wave % a.hpw);
-  const int g = (hg * a.hpw) / G;
-  const int sub = wave / a.hpw;
-  const int nA = L / a.gamma;
+  // hpw is a power of two: head in block = wave % hpw, sub-tile = wave / hpw
+  const int hpw_log = __builtin_ctz(a.hpw);
+  const int h = hg * a.hpw + (wave & (a.hpw - 1));
+  const int g = (int)fdiv((uint32_t)(hg * a.hpw), a.fd_G);
+  const int sub = wave >> hpw_log;
+  const int nA = (int)fdiv((uint32_t)L, a.fd_gamma);
   const int Lc = nA * a.gamma;
   const int n_rows = (MODE == kDenseRows) ? nA + (L - Lc) : L;
 
@@ -204,7 +210,7 @@ void attn_kernel(Args a) {
   // block's tiles [diag0, last row's tile]
   int lst0 = 0, diag0 = 0;
   if (MODE == kSparse && a.blk_ptr) {
-    const int qb = R0 / a.block_q;  // the block's rows lie in one query block
+    const int qb = (int)fdiv((uint32_t)R0, a.fd_bq);  // the block's rows lie in one query block
     const int64_t pi = ((int64_t)b * a.Hkv + g) * (a.nqb + 1) + qb;
     lst0 = a.blk_ptr[pi];
     ta1 = max(0, a.blk_ptr[pi + 1] - lst0);
@@ -245,42 +251,7 @@ void attn_kernel(Args a) {
   const int wpos_hi = wave_has_rows ? row_pos<MODE>(min(wr0 + kRowsPerWave, R1) - 1, nA, Lc,
                                                     a.gamma) : -1;
 
-  // Q fragments: lane holds dims kk*16 + half*8 .. +8 of its row, for every kk.
-  // Rows past the end of the block load row R1-1's query (a valid row) and are
-  // never written, so no load sits behind a branch.
-  bf16x8 qf[D / 16];
-  {
-    const int pos_ld = row_valid ? my_pos : row_pos<MODE>(R1 - 1, nA, Lc, a.gamma);
-    const uint16_t* qp = a.q + ((sq.base + pos_ld) * a.Hq + h) * (int64_t)D + half * 8;
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + kk * 16);
-    // Fused store: fetch the merged dense rows of the block's anchors whose
-    // Delta is not zero (anchor slot = head in block * groups per slab +
-    // group in slab), so the epilogue does not wait on memory.
-    if (MODE == kSparse && a.fuse && a.gamma > 1) {
-      const int per_slab = kRowsPerWave * a.ppw / a.gamma;
-      const int a_end = min(R1, Lc);
-      const int nvec = a.hpw * per_slab * (D / 4);
-      for (int u = tid; u < nvec; u += kAttnThreads) {
-        const int slot = u / (D / 4), dv = u % (D / 4);
-        const int apos = R0 + (slot % per_slab) * a.gamma;
-        if (apos < a_end && (int64_t)apos >= a.cover) {
-          const int hh = hg * a.hpw + slot / per_slab;
-          *(f32x4*)(dpre + slot * D + dv * 4) = *(const f32x4*)(
-              a.dense + (((int64_t)b * a.Hq + hh) * a.nR_max + apos / a.gamma) * D + dv * 4);
-        }
-      }
-    }
-    // retire the Q loads here (vmcnt(0)): the main loop's MFMAs read qf every
-    // iteration and must not wait behind the prefetch loads issued in it
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-  }
-  // Queries pre-scaled by log2(e)/sqrt(d) and rounded to bf16 once, so the
-  // score accumulators hold base-2 logits and the weights need no multiply.
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk)
-    qf[kk] = __builtin_convertvector(__builtin_convertvector(qf[kk], f32x8) * a.scale_log2, bf16x8);
-
+  bf16x8 qf[D / 16];  // the wave's queries (loaded in the prologue below)
   const int64_t kv_stride = (int64_t)a.Hkv * D;  // elements between consecutive keys
   const uint16_t* kbase = a.k + (sq.base * a.Hkv + g) * (int64_t)D;
   const uint16_t* vbase = a.v + (sq.base * a.Hkv + g) * (int64_t)D;
@@ -361,17 +332,22 @@ void attn_kernel(Args a) {
   };
 
   // 0: no key of the tile is visible to any row of the wave; 1: every key is
-  // visible to every row; 2: mixed, mask per element.
+  // visible to every row; otherwise the mask the tile needs per element:
+  // kMaskCausal (some key lies past some row), kMaskWindow (some key lies
+  // before some row's window), kMaskBoth, or kMaskAll (the window test meets
+  // sink keys).  The dense modes only ever need the causal mask.
   auto classify = [&](int tile) -> int {
     if (!wave_has_rows || tile < 0) return 0;
     const int k0 = tile * kKeyTile, k1 = k0 + kKeyTile - 1;
     if (k0 > wpos_hi) return 0;
     if (MODE == kSparse) {
       if (k0 >= a.n_sink && wpos_lo - k1 >= a.window) return 0;
-      const bool full = k1 <= wpos_lo && (k1 < a.n_sink || wpos_hi - k0 < a.window);
-      return full ? 1 : 2;
+      const bool need_c = k1 > wpos_lo;
+      const bool need_w = k1 >= a.n_sink && (int64_t)wpos_hi - k0 >= a.window;
+      if (need_w && k0 < a.n_sink) return kMaskAll;
+      return need_c ? (need_w ? kMaskBoth : kMaskCausal) : (need_w ? kMaskWindow : 1);
     }
-    return k1 <= wpos_lo ? 1 : 2;
+    return k1 <= wpos_lo ? 1 : kMaskCausal;
   };
 
   f32x16 o[D / 32];
@@ -390,7 +366,7 @@ void attn_kernel(Args a) {
   // S^T of one tile against the wave's rows (register r of lane half h holds
   // key 8*(r/4) + 4*h + r%4 in s0, that key + 32 in s1); keys outside a row's
   // key set read -inf when `masked`.
-  auto qk = [&](const uint16_t* ks, int tile, bool masked, f32x16& s0, f32x16& s1) {
+  auto qk = [&](const uint16_t* ks, int tile, int masked, f32x16& s0, f32x16& s1) {
     s0 = nref;
     s1 = nref;
 #pragma unroll
@@ -420,18 +396,24 @@ void attn_kernel(Args a) {
       // so a bound clamped at -1 admits the whole tile, as such a window does)
       const int lim_w = (int)max((int64_t)lim_c - (int64_t)a.window, (int64_t)-1);
       const int lim_s = a.n_sink - kbase_t;
+      // one element test per mask kind (the kind is wave-uniform in the sparse
+      // mode, so each is a branch of its own)
+      auto apply = [&](auto ok) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int o0 = 8 * (r >> 2) + (r & 3);
-        const int o1 = o0 + 32;
-        bool ok0 = o0 <= lim_c, ok1 = o1 <= lim_c;
-        if (MODE == kSparse) {
-          ok0 = ok0 && (o0 < lim_s || o0 > lim_w);
-          ok1 = ok1 && (o1 < lim_s || o1 > lim_w);
+        for (int r = 0; r < 16; ++r) {
+          const int o0 = 8 * (r >> 2) + (r & 3);
+          s0[r] = ok(o0) ? s0[r] : -INFINITY;
+          s1[r] = ok(o0 + 32) ? s1[r] : -INFINITY;
         }
-        s0[r] = ok0 ? s0[r] : -INFINITY;
-        s1[r] = ok1 ? s1[r] : -INFINITY;
-      }
+      };
+      if (MODE != kSparse || masked == kMaskCausal)
+        apply([&](int o) { return o <= lim_c; });
+      else if (masked == kMaskWindow)
+        apply([&](int o) { return o > lim_w; });
+      else if (masked == kMaskBoth)
+        apply([&](int o) { return o <= lim_c && o > lim_w; });
+      else
+        apply([&](int o) { return o <= lim_c && (o < lim_s || o > lim_w); });
     }
   };
 
@@ -548,7 +530,7 @@ void attn_kernel(Args a) {
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   };
 
-  auto compute = [&](const uint16_t* ks, int tile, bool masked) {
+  auto compute = [&](const uint16_t* ks, int tile, int masked) {
     f32x16 s0, s1;
     bf16x8 pf[4];
     qk(ks, tile, masked, s0, s1);
@@ -556,19 +538,69 @@ void attn_kernel(Args a) {
     pv(ks + LD::kElems, pf);
   };
 
+  // ---- prologue: the first tile's DMA, the queries and the staged dense rows
+  // are all in flight before the block waits once for them.
+  //
+  // A stage holds the tile of its last DMA; lanes past the sequence end are
+  // written as zeros.  Only a block whose first NS tiles include its last one
+  // (the only tile that can end inside the sequence's last 64 keys) clears
+  // the ring first, so that no stage can hold bits left by an earlier kernel.
+  if (n_iter <= NS) {
+    for (int i = tid; i < NS * LD::stageElems / 8; i += kAttnThreads)
+      *(u32x4*)(smem + 8 * i) = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  }
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < n_iter) dma(tile_at(p), p);
+
+  // Q fragments: lane holds dims kk*16 + half*8 .. +8 of its row, for every kk.
+  // Rows past the end of the block load row R1-1's query (a valid row) and are
+  // never written, so no load sits behind a branch.
+  {
+    const int pos_ld = row_valid ? my_pos : row_pos<MODE>(R1 - 1, nA, Lc, a.gamma);
+    const uint16_t* qp = a.q + ((sq.base + pos_ld) * a.Hq + h) * (int64_t)D + half * 8;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + kk * 16);
+  }
+  // Fused store: the merged dense rows of the block's anchors whose Delta is
+  // not zero (anchor slot = head in block * groups per slab + group in slab),
+  // staged in LDS so the epilogue does not wait on memory.  Each thread's
+  // first vector loads with the queries; gamma < 16 (d = 128) leaves more.
+  const bool stage_dense = MODE == kSparse && a.fuse && a.gamma > 1;
+  const int per_slab = (int)fdiv((uint32_t)(kRowsPerWave * a.ppw), a.fd_gamma);
+  const int nvec = stage_dense ? a.hpw * per_slab * (D / 4) : 0;
+  auto dense_src = [&](int u) -> const f32x4* {
+    const int slot = u / (D / 4), dv = u % (D / 4);
+    const int apos = R0 + (slot % per_slab) * a.gamma;
+    if (apos >= min(R1, Lc) || (int64_t)apos < a.cover) return nullptr;
+    const int hh = hg * a.hpw + slot / per_slab;
+    return (const f32x4*)(a.dense + (((int64_t)b * a.Hq + hh) * a.nR_max +
+                                     (int)fdiv((uint32_t)apos, a.fd_gamma)) * D + dv * 4);
+  };
+  const f32x4* dsrc = tid < nvec ? dense_src(tid) : nullptr;
+  f32x4 dreg = f32x4{};
+  if (dsrc) dreg = *dsrc;
+  // Everything above has landed after this wait (vmcnt(0)): the main loop's
+  // MFMAs read qf every iteration and must not wait behind the DMA issued in
+  // it, and the first tile is in this wave's part of stage 0.
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  if (dsrc) *(f32x4*)(dpre + tid * 4) = dreg;
+  for (int u = tid + kAttnThreads; u < nvec; u += kAttnThreads)
+    if (const f32x4* src = dense_src(u)) *(f32x4*)(dpre + u * 4) = *src;
+  // Queries pre-scaled by log2(e)/sqrt(d) and rounded to bf16 once, so the
+  // score accumulators hold base-2 logits and the weights need no multiply.
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk)
+    qf[kk] = __builtin_convertvector(__builtin_convertvector(qf[kk], f32x8) * a.scale_log2, bf16x8);
+
   // ---- main loop over a ring of NS LDS stages, one barrier per tile.  Step
   // `it` waits until this wave's DMA of tile it has landed (later tiles may
   // still be in flight), meets the other waves at the barrier (after which
   // tile it is in LDS for everyone and nobody reads stage (it-1) % NS any
   // more), starts the DMA of tile it+NS-1 into that stage, then computes
-  // tile it.  LDS starts zeroed, so no stage ever holds non-finite bits (keys
-  // past the sequence end arrive as zeros from the DMA).
-  for (int i = tid; i < NS * LD::stageElems / 8; i += kAttnThreads)
-    *(u32x4*)(smem + 8 * i) = u32x4{0u, 0u, 0u, 0u};
-  __syncthreads();
-#pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < n_iter) dma(tile_at(p), p);
+  // tile it.  Keys past the sequence end arrive as zeros from the DMA; a
+  // stage is read only after a DMA has filled it.
   constexpr int kLoadsPerTile = 2 * RPW;  // vmcnt entries one tile's DMA adds per wave
   // The loop is unrolled by the ring depth so each step's stage is a constant:
   // the LDS operand addresses are then a loop-invariant per-lane register plus
@@ -595,11 +627,11 @@ void attn_kernel(Args a) {
         // mask as a branch inside it, so the accumulators keep one register
         // assignment across tiles (two copies made the compiler copy O
         // between them at every step)
-        if (cls != 0) compute(ks, tile, cls == 2);
+        if (cls != 0) compute(ks, tile, cls == 1 ? 0 : cls);
       } else if (cls == 1) {
-        compute(ks, tile, false);
-      } else if (cls == 2) {
-        compute(ks, tile, true);
+        compute(ks, tile, 0);
+      } else if (cls != 0) {
+        compute(ks, tile, kMaskCausal);
       }
     }
   }
@@ -620,12 +652,13 @@ void attn_kernel(Args a) {
     // untouched.  Recompute (fuse 2) replaces anchors only.
     const float inv = 1.f / lt;
     const bool in_c = row_valid && my_pos < Lc;
-    const int anc = in_c ? my_pos - my_pos % a.gamma : 0;
+    // group of the row inside the block's slab (R0 is a multiple of gamma)
+    const int grp = in_c ? (int)fdiv((uint32_t)(my_pos - R0), a.fd_gamma) : 0;
+    const int anc = in_c ? R0 + grp * a.gamma : 0;
     const bool open = in_c && (int64_t)anc >= a.cover;
     const bool is_anchor = open && anc == my_pos;
     const bool staged = a.gamma > 1;  // anchor dense rows are in dpre
-    const int xslot =
-        ((wave % a.hpw) * (kRowsPerWave * a.ppw / a.gamma) + (in_c ? (my_pos - R0) / a.gamma : 0)) * D;
+    const int xslot = ((wave & (a.hpw - 1)) * per_slab + grp) * D;
     uint16_t* orow = a.out + ((sq.base + (row_valid ? my_pos : 0)) * a.Hq + h) * (int64_t)D;
     if (a.fuse == 1 && staged) {
       if (is_anchor) {
@@ -648,29 +681,53 @@ void attn_kernel(Args a) {
     const bool tail = my_pos >= Lc;
     const bool add = a.fuse == 1 && staged && open;
     const float* gdrow =  // dense row in global memory: tail rows, and anchors when not staged
-        a.dense + (((int64_t)b * a.Hq + h) * a.nR_max + (in_c ? my_pos / a.gamma : nA + (my_pos - Lc))) * D;
+        a.dense + (((int64_t)b * a.Hq + h) * a.nR_max + (in_c ? (int)fdiv((uint32_t)my_pos, a.fd_gamma)
+                                                                : nA + (my_pos - Lc))) * D;
+    // one branch per row kind (not one per vector): corrected rows fold the
+    // normalisation into the add, sparse rows only normalise, dense rows copy
+    f32x4 val[D / 32][4];
+    if (add) {
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) {
+      for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int dim = 32 * mb + 8 * jq + 4 * half;
-        f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
-                     o[mb][4 * jq + 3] * inv};
-        if (tail || (is_anchor && !staged)) val = *(const f32x4*)(gdrow + dim);
-        else if (is_anchor) val = *(const f32x4*)(dpre + xslot + dim);
-        else if (add) val += *(const f32x4*)(dpre + xslot + dim);
-        *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
-      }
+        for (int jq = 0; jq < 4; ++jq) {
+          const f32x4 dl = *(const f32x4*)(dpre + xslot + 32 * mb + 8 * jq + 4 * half);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) val[mb][jq][e] = __builtin_fmaf(o[mb][4 * jq + e], inv, dl[e]);
+        }
+    } else if (tail || (is_anchor && !staged)) {
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq) val[mb][jq] = *(const f32x4*)(gdrow + 32 * mb + 8 * jq + 4 * half);
+    } else if (is_anchor) {
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq)
+          val[mb][jq] = *(const f32x4*)(dpre + xslot + 32 * mb + 8 * jq + 4 * half);
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+        for (int jq = 0; jq < 4; ++jq)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) val[mb][jq][e] = o[mb][4 * jq + e] * inv;
     }
+#pragma unroll
+    for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq)
+        *(bf16x4*)(orow + 32 * mb + 8 * jq + 4 * half) = __builtin_convertvector(val[mb][jq], bf16x4);
     return;
   }
   if (!row_valid) return;
   if (MODE != kDenseRows) {
     const float inv = 1.f / lt;
     uint16_t* orow = a.out + ((sq.base + my_pos) * a.Hq + h) * (int64_t)D;
-    const bool write_sa = (MODE == kSparse) && a.sa && (my_pos % a.gamma == 0) && my_pos < Lc;
-    float* sarow = write_sa ? a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + my_pos / a.gamma) * D
-                            : nullptr;
+    const int grp = (MODE == kSparse && a.sa) ? (int)fdiv((uint32_t)my_pos, a.fd_gamma) : 0;
+    const bool write_sa = (MODE == kSparse) && a.sa && grp * a.gamma == my_pos && my_pos < Lc;
+    float* sarow = write_sa ? a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + grp) * D : nullptr;
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb) {
 #pragma unroll
@@ -987,8 +1044,15 @@ __global__ __launch_bounds__(256) void check_inputs_kernel(const int32_t* cu, in
 }
 
 template <int MODE>
-hipError_t launch_attn(const Args& a, hipStream_t s, int64_t nblocks) {
+hipError_t launch_attn(const Args& a0, hipStream_t s, int64_t nblocks) {
   if (nblocks <= 0) return hipSuccess;
+  Args a = a0;
+  a.fd_rtiles = make_fastdiv((uint32_t)a.n_rtiles);
+  a.fd_nC = make_fastdiv((uint32_t)(a.nC > 0 ? a.nC : 1));
+  a.fd_B = make_fastdiv((uint32_t)a.B);
+  a.fd_G = make_fastdiv((uint32_t)(a.Hq / a.Hkv));
+  a.fd_gamma = make_fastdiv((uint32_t)a.gamma);
+  a.fd_bq = make_fastdiv((uint32_t)(a.block_q > 0 ? a.block_q : 1));
   if (a.d == 128)
     hipLaunchKernelGGL((attn_kernel<128, MODE>), dim3((unsigned)nblocks), dim3(kAttnThreads), 0, s, a);
   else
