@@ -53,36 +53,26 @@ def pair_counts(seqlens, window, n_sink, gamma):
     return sp, dr, dc
 
 
-def heads_per_block(G):
-    """Query heads sharing an attention workgroup: the largest power of two
-    dividing G, at most 8 (one wavefront of 32 rows per head and sub-tile)."""
-    h = 1
-    while h * 2 <= 8 and G % (h * 2) == 0:
-        h *= 2
-    return h
+def launch_plan(wl, block_q=0):
+    """The library's own tiling of this workload (da_launch_plan, host only)."""
+    from paper_2505_11254_amd import binding
+    return binding.launch_plan(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma, block_q)
 
 
-def fused_heads_per_block(G, gamma):
-    h = heads_per_block(G)
-    while h >= 1:
-        if G % h == 0 and (32 * (8 // h)) % gamma == 0:
-            return h
-        h //= 2
-    return 0
-
-
-def executed_pairs(wl, kind, hpw=None):
+def executed_pairs(wl, kind, plan=None):
     """Per head: (row, key) pairs the MFMAs execute, whole tiles counted, as the
-    kernels tile the work.  A workgroup holds hpw heads x (8 / hpw) wavefronts
-    of 32 rows; a wavefront runs every 64-key tile of its workgroup's range
-    in which some key is visible to some of its rows and skips the others.
-    kind: "sparse" (sink + window rows), "dense_rows" (anchors and tail rows,
-    key axis split in chunks) or "dense" (every row, causal)."""
+    kernels tile the work (the library's plan, `launch_plan`).  A workgroup
+    holds hpw heads x (8 / hpw) wavefronts of 32 rows; a wavefront runs every
+    64-key tile of its workgroup's range in which some key is visible to some
+    of its rows and skips the others.  kind: "sparse" (sink + window rows, in
+    the schedule the whole-path call takes), "dense_rows" (anchors and tail
+    rows, key axis split in chunks) or "dense" (every row, causal)."""
     import numpy as np
-    G = wl.Hq // wl.Hkv
-    hpw = hpw or heads_per_block(G)
+    plan = plan or launch_plan(wl)
+    assert (plan["key_tile"], plan["rows_per_wave"], plan["waves_per_block"]) == (64, 32, 8)
+    hpw = plan["sparse_heads"] if kind == "sparse" else plan["rows_heads"]
     ppw = 8 // hpw
-    chunk = plan_chunk(wl)
+    chunk = plan["chunk_keys"]
     tot = 0
     for L in wl.seqlens:
         nA = L // wl.gamma
@@ -146,25 +136,12 @@ def epilogue_bytes(wl, cover):
     return tot
 
 
-def plan_chunk(wl):
-    """Keys per key chunk of the strided dense rows, as the library plans it:
-    ceil(max_seqlen / 2048) chunks, at most 16 (fewer only when the partial
-    results would pass 8 GiB), rounded up to a multiple of 64 keys."""
-    L = wl.max_seqlen
-    nA = L // wl.gamma
-    nR = nA + min(wl.gamma - 1, L)
-    nC = max(1, min(16, -(-L // 2048)))
-    while nC > 1 and wl.B * wl.Hq * nR * (wl.d + 2) * 4 * nC > (8 << 30):
-        nC -= 1
-    return -(-(-(-L // nC)) // 64) * 64
-
-
 def merge_bytes(wl, cover):
     """Algorithmic HBM bytes of the fused schedule's merge: for every dense row
     it merges (anchors a >= cover, whose Delta is not zero, and tail rows), read
     the fp32 partial (d values, max, normaliser) of each key chunk the row
     reaches and write the merged fp32 row."""
-    chunk = plan_chunk(wl)
+    chunk = launch_plan(wl)["chunk_keys"]
     tot = 0
     first_open = -(-cover // wl.gamma)
     for L in wl.seqlens:
@@ -195,6 +172,18 @@ def load_traffic(kernel, workload):
     if not ent or ent.get("source_hash") != kernel_source_hash():
         return None
     return ent.get("bytes_per_launch")
+
+
+def cpu_model():
+    """The host CPU's model name (first `model name` line of /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_baseline(wl, q, k, v, target_s=12.0):
@@ -249,6 +238,7 @@ def cpu_baseline(wl, q, k, v, target_s=12.0):
     tokens = wl.total_tokens
     return {
         "value": tokens / t_full, "unit": "tokens/s", "cores": nthreads, "kind": "oracle",
+        "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
         "sample": (f"{n_sp} sparse rows ({k_sp} keys) and {n_dn} anchor dense rows "
                    f"({k_dn} keys), random heads/positions of this workload, timed "
                    f"{spent:.1f} s; whole-workload time {t_full:.0f} s extrapolated by exact "
@@ -287,9 +277,10 @@ BASES = {
 
 
 def other_workload(binding, generate, wl, dev, steps, with_dense):
-    """The metric is quoted at 131K as well as 1M: the whole Delta path
-    (delta_attn_prefill) on another workload, with the dense causal baseline,
-    timed with HIP events on the launch stream."""
+    """Another workload of the metric (131K, 32K, ragged batch): the whole
+    Delta path in the schedule delta_attn_prefill takes, one kernel per call
+    with HIP events between them on the launch stream, the dense causal
+    baseline, and each MFMA kernel's executed and useful flop rates."""
     import torch
     q, k, v, cu = generate(wl, device=dev)
     kw = dict(B=wl.B) if wl.fixed_length else dict(cu_seqlens=cu, max_seqlen=wl.max_seqlen)
@@ -297,22 +288,56 @@ def other_workload(binding, generate, wl, dev, steps, with_dense):
     ws = torch.empty(binding.workspace_bytes(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma),
                      dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
-    run = lambda: binding.delta_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink,
-                                            gamma=wl.gamma, out=out, workspace=ws, **kw)
+    plan = launch_plan(wl)
+    F = binding.STEP_FUSED
+    order = ([("strided_dense_rows", binding.STEP_DENSE_ROWS | F),
+              ("dense_row_merge", binding.STEP_CORRECT | F), ("sparse_window", binding.STEP_SPARSE | F)]
+             if plan["fused"] else
+             [("sparse_window", binding.STEP_SPARSE), ("strided_dense_rows", binding.STEP_DENSE_ROWS),
+              ("delta_epilogue", binding.STEP_CORRECT)])
+    pkw = dict(window=wl.window, n_sink=wl.n_sink, gamma=wl.gamma, B=wl.B,
+               cu_seqlens=None if wl.fixed_length else cu, max_seqlen=wl.max_seqlen)
+
+    def step(evs=None):
+        for i, (_, bits) in enumerate(order):
+            if evs is not None:
+                evs[i].record(stream)
+            binding.delta_attn_prefill_steps(q, k, v, out, ws, bits, **pkw)
+        if evs is not None:
+            evs[len(order)].record(stream)
+
     n, t0 = 0, time.perf_counter()
     while n < 2 or time.perf_counter() - t0 < 0.5:
-        run()
+        step()
         torch.cuda.synchronize()
         n += 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(order) + 1)]
+           for _ in range(steps)]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     e0.record(stream)
-    for _ in range(steps):
-        run()
+    for s_ in range(steps):
+        step(evs[s_])
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
+    k_ms = {name: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / steps
+            for i, (name, _) in enumerate(order)}
+    sp, dr, dc = pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
+    fl = lambda pairs: 4.0 * wl.d * wl.Hq * pairs
+    kinds = {"sparse_window": ("sparse", sp), "strided_dense_rows": ("dense_rows", dr)}
+    kernels = {}
+    for name, t in k_ms.items():
+        kernels[name] = {"ms": round(t, 4)}
+        if name in kinds:
+            kind, pairs = kinds[name]
+            x = fl(executed_pairs(wl, kind, plan)) / t / 1e9
+            kernels[name].update(executed_tflops=round(x, 2),
+                                 useful_tflops=round(fl(pairs) / t / 1e9, 2),
+                                 mfma_frac=round(x / PEAK_BF16_TFLOPS, 4))
     rec = {"ms_per_step": round(ms, 4), "tokens_per_s": round(wl.total_tokens / (ms / 1e3), 1),
-           "steps": steps, "warmup": n, "dense_causal_ms": None, "speedup_vs_dense_causal": None}
+           "steps": steps, "warmup": n, "schedule": "fused" if plan["fused"] else "unfused",
+           "kernels": kernels, "dense_causal_ms": None, "speedup_vs_dense_causal": None}
     if with_dense:
         binding.dense_causal_attn_prefill(q, k, v, out=out, **kw)
         torch.cuda.synchronize()
@@ -323,8 +348,15 @@ def other_workload(binding, generate, wl, dev, steps, with_dense):
         dms = e0.elapsed_time(e1)
         rec["dense_causal_ms"] = round(dms, 3)
         rec["speedup_vs_dense_causal"] = round(dms / ms, 2)
+        x = fl(executed_pairs(wl, "dense", plan)) / dms / 1e9
+        kernels["dense_causal"] = {"ms": round(dms, 3), "executed_tflops": round(x, 2),
+                                   "useful_tflops": round(fl(dc) / dms / 1e9, 2),
+                                   "mfma_frac": round(x / PEAK_BF16_TFLOPS, 4)}
     log(f"{wl.name}: delta path {ms:.3f} ms/step ({rec['tokens_per_s']:.0f} tokens/s), "
-        f"dense causal {rec['dense_causal_ms']} ms")
+        + ", ".join(f"{nm} {t:.3f} ms" for nm, t in k_ms.items())
+        + f", dense causal {rec['dense_causal_ms']} ms")
+    del q, k, v, out, ws
+    torch.cuda.empty_cache()
     return rec
 
 
@@ -510,9 +542,10 @@ def main():
                     help="time only the Delta path (and the dense baseline unless --no-dense): "
                          "skip the unfused-schedule and sparse-only comparison runs, so a "
                          "profiled run holds the path's own launches")
-    ap.add_argument("--no-131k", action="store_true",
-                    help="skip the second workload the metric is quoted on (the 131K layer), "
-                         "timed after the headline one")
+    ap.add_argument("--no-others", "--no-131k", dest="no_others", action="store_true",
+                    help="skip the other workloads timed after the headline one (the 131K "
+                         "layer the metric is also quoted on, the 32K layer and the ragged "
+                         "batch)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy a 1 GiB device buffer, a dispatch of known traffic "
                          "against which HBM byte counters are scaled")
@@ -707,12 +740,11 @@ def run_main(args, sampler):
     flops = {"sparse": fl(sp_pairs), "dense_rows": fl(dr_pairs), "dense_causal": fl(dc_pairs)}
     # executed flops: whole tiles the MFMAs run, as the kernels tile the work
     # (sink + window basis only; key-block lists are counted as useful flops)
-    G = wl.Hq // wl.Hkv
-    xflops = {"dense_rows": fl(executed_pairs(wl, "dense_rows")),
-              "dense_causal": fl(executed_pairs(wl, "dense"))}
+    plan = launch_plan(wl)
+    xflops = {"dense_rows": fl(executed_pairs(wl, "dense_rows", plan)),
+              "dense_causal": fl(executed_pairs(wl, "dense", plan))}
     if args.basis == "streaming":
-        xflops["sparse"] = fl(executed_pairs(
-            wl, "sparse", fused_heads_per_block(G, wl.gamma) if fused else heads_per_block(G)))
+        xflops["sparse"] = fl(executed_pairs(wl, "sparse", plan))
 
     # dense causal baseline (the in-house quadratic kernel)
     dense_ms = None
@@ -737,9 +769,12 @@ def run_main(args, sampler):
         del out_d
 
     def rates(key, ms):
+        # MFMA kernels: useful and executed flop rates, and the executed rate's
+        # fraction of the bf16 MFMA peak
         r = {"ms": ms, "useful_tflops": flops[key] / ms / 1e9}
         if key in xflops:
             r["executed_tflops"] = xflops[key] / ms / 1e9
+            r["mfma_frac"] = r["executed_tflops"] / PEAK_BF16_TFLOPS
         return r
 
     per_kernel = {SP: rates("sparse", k_ms[SP]),
@@ -790,14 +825,14 @@ def run_main(args, sampler):
     # headline workload's tensors are released)
     also = None
     if (wl.name == HEADLINE and args.basis == "streaming" and not args.path_only
-            and not args.no_131k):
+            and not args.no_others):
         del q, k, v, out
         if "ws" in locals():
             del ws
         torch.cuda.empty_cache()
-        also = {"llama8b_layer_131k": other_workload(binding, generate,
-                                                      WORKLOADS["llama8b_layer_131k"], dev,
-                                                      max(args.steps, 20), not args.no_dense)}
+        also = {name: other_workload(binding, generate, WORKLOADS[name], dev,
+                                     max(args.steps, 20), not args.no_dense)
+                for name in ("llama8b_layer_131k", "llama8b_layer_32k", "ragged_b4_gqa8")}
 
     value = T / (ms_per_step / 1e3)
     rec = {

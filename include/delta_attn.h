@@ -275,6 +275,33 @@ da_status da_check_inputs(const int32_t* cu_seqlens, int B, int max_seqlen, int 
                           const int32_t* block_ptr, const int32_t* block_idx, int64_t block_nnz,
                           int32_t* result, void* stream);
 
+/*
+ * How the library tiles a problem, as the launch sequence of
+ * delta_attn_prefill[_varlen] uses it (block_q = 0), or of the key-block-list
+ * calls (block_q = 64, 128 or 256): a host-only query, no HIP call.  A caller
+ * counts the work the kernels execute (whole tiles of key_tile keys by
+ * rows_per_wave query rows per wavefront) from these numbers instead of
+ * restating the plan.  Each attention workgroup holds waves_per_block
+ * wavefronts: heads query heads of one GQA group, each with waves_per_block /
+ * heads row sub-tiles of rows_per_wave rows.  The strided dense rows split
+ * their key axis into key_chunks chunks of chunk_keys keys.
+ * Returns DA_ERR_NULL without `plan`, otherwise the status the whole-path
+ * call would return for these sizes before touching the device.
+ */
+typedef struct {
+  int fused;            /* 1: the whole-path call takes the fused schedule */
+  int sparse_heads;     /* query heads per sparse workgroup in that schedule */
+  int rows_heads;       /* query heads per strided-row (and dense causal) workgroup */
+  int key_chunks;       /* key chunks of the strided dense rows */
+  int chunk_keys;       /* keys per chunk, a multiple of key_tile */
+  int key_tile;         /* keys per tile */
+  int rows_per_wave;    /* query rows per wavefront */
+  int waves_per_block;  /* wavefronts per attention workgroup */
+} da_plan;
+
+da_status da_launch_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, int block_q,
+                         da_plan* plan);
+
 /* Static, NUL-terminated name of a status code. */
 const char* da_status_string(da_status s);
 

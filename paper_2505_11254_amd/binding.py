@@ -38,6 +38,16 @@ SIGNATURES = {
 }
 
 
+class Plan(ctypes.Structure):
+    """da_plan of include/delta_attn.h: how the library tiles a problem."""
+    _fields_ = [(n, ctypes.c_int) for n in ("fused", "sparse_heads", "rows_heads", "key_chunks",
+                                            "chunk_keys", "key_tile", "rows_per_wave",
+                                            "waves_per_block")]
+
+    def as_dict(self):
+        return {n: int(getattr(self, n)) for n, _ in self._fields_}
+
+
 class DeltaAttnError(RuntimeError):
     def __init__(self, fn, status, hip_error=0):
         self.status = status
@@ -80,6 +90,8 @@ def load_library(path: str = LIB_PATH):
     lib.da_last_hip_error.restype = ctypes.c_int
     lib.da_abi_version.argtypes = []
     lib.da_abi_version.restype = ctypes.c_int
+    lib.da_launch_plan.argtypes = [ctypes.c_int] * 7 + [ctypes.POINTER(Plan)]
+    lib.da_launch_plan.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -100,10 +112,59 @@ def _stream(device, stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _shapes(q, k, v, B, cu_seqlens, max_seqlen):
+def _on_device(name, t, dev, dtype):
+    """t must be a contiguous tensor of `dtype` on the GPU `dev` (the kernels
+    dereference its pointer on that device)."""
+    if not getattr(t, "is_cuda", False) or t.device != dev:
+        raise ValueError(f"{name} must be on {dev} (got {t.device})")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _span(t):
+    n = t.numel() * t.element_size()
+    return t.data_ptr(), t.data_ptr() + n
+
+
+def _check(q, k, v, out=None, cu_seqlens=None, workspace=None, block_ptr=None,
+           block_idx=None):
+    """Everything the C ABI takes on trust about the tensors behind its
+    pointers: device, dtype, layout, matching shapes and no aliasing of the
+    output with an input.  Raises ValueError before anything is launched."""
+    dev = q.device
     for name, t in (("q", q), ("k", k), ("v", v)):
+        _on_device(name, t, dev, torch.bfloat16)
         if t.dim() != 3:
             raise ValueError(f"{name} must be [T, H, d]")
+    if tuple(k.shape) != tuple(v.shape):
+        raise ValueError(f"k and v must have the same shape (got {tuple(k.shape)} and "
+                         f"{tuple(v.shape)})")
+    if k.shape[0] != q.shape[0] or k.shape[2] != q.shape[2]:
+        raise ValueError("k and v must be [T, Hkv, d] with the T and d of q")
+    if out is not None:
+        _on_device("out", out, dev, torch.bfloat16)
+        if tuple(out.shape) != tuple(q.shape):
+            raise ValueError(f"out must have the shape of q {tuple(q.shape)}")
+        o0, o1 = _span(out)
+        for name, t in (("q", q), ("k", k), ("v", v)):
+            t0, t1 = _span(t)
+            if o0 < t1 and t0 < o1:
+                raise ValueError(f"out must not overlap {name}")
+    if cu_seqlens is not None:
+        _on_device("cu_seqlens", cu_seqlens, dev, torch.int32)
+        if cu_seqlens.dim() != 1 or cu_seqlens.numel() < 2:
+            raise ValueError("cu_seqlens must be 1-D with B + 1 >= 2 entries")
+    if workspace is not None:
+        _on_device("workspace", workspace, dev, None)
+    for name, t in (("block_ptr", block_ptr), ("block_idx", block_idx)):
+        if t is not None:
+            _on_device(name, t, dev, torch.int32)
+
+
+def _shapes(q, k, v, B, cu_seqlens, max_seqlen):
+    _check(q, k, v, cu_seqlens=cu_seqlens)
     T, Hq, d = q.shape
     Hkv = k.shape[1]
     if cu_seqlens is None:
@@ -113,13 +174,21 @@ def _shapes(q, k, v, B, cu_seqlens, max_seqlen):
         return B, T // B, Hq, Hkv, d
     if max_seqlen is None:
         raise ValueError("max_seqlen is required with cu_seqlens")
-    if cu_seqlens.dtype != torch.int32:
-        raise ValueError("cu_seqlens must be int32")
     return cu_seqlens.numel() - 1, int(max_seqlen), Hq, Hkv, d
 
 
 def workspace_bytes(B, max_seqlen, Hq, Hkv, d, gamma) -> int:
     return int(load_library().da_workspace_bytes(B, max_seqlen, Hq, Hkv, d, gamma))
+
+
+def launch_plan(B, max_seqlen, Hq, Hkv, d, gamma, block_q=0) -> dict:
+    """The library's tiling of a problem (da_launch_plan; host only)."""
+    p = Plan()
+    lib = load_library()
+    rc = lib.da_launch_plan(B, max_seqlen, Hq, Hkv, d, gamma, block_q, ctypes.byref(p))
+    if rc != 0:
+        raise DeltaAttnError("da_launch_plan", rc)
+    return p.as_dict()
 
 
 def fused_supported(Hq, Hkv, gamma) -> bool:
@@ -136,6 +205,7 @@ def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=Non
     nbytes = workspace_bytes(B_, N, Hq, Hkv, d, gamma)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    _check(q, k, v, out, cu_seqlens, workspace)
     wsz = workspace.numel() * workspace.element_size()
     st = _stream(q.device, stream)
     if cu_seqlens is None:
@@ -162,6 +232,7 @@ def delta_attn_prefill_correction(q, k, v, *, window, n_sink, gamma, mode,
     nbytes = int(load_library().da_workspace_bytes_correction(B_, N, Hq, Hkv, d, gamma, mode))
     if workspace is None:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    _check(q, k, v, out, cu_seqlens, workspace)
     wsz = workspace.numel() * workspace.element_size()
     p = list(params) + [0.0] * (3 - len(params))
     _call("delta_attn_prefill_correction", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
@@ -174,6 +245,7 @@ def delta_attn_prefill_steps(q, k, v, out, workspace, steps, *, window, n_sink, 
                              cu_seqlens=None, max_seqlen=None, stream=None):
     """Run the given steps of Algorithm 1 (bit mask of STEP_*) on existing buffers."""
     B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    _check(q, k, v, out, cu_seqlens, workspace)
     wsz = workspace.numel() * workspace.element_size()
     _call("delta_attn_prefill_steps", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(cu_seqlens),
           B_, N, Hq, Hkv, d, window, n_sink, gamma, _ptr(workspace), wsz,
@@ -187,6 +259,7 @@ def sparse_attn_prefill(q, k, v, *, window, n_sink, B=None, cu_seqlens=None, max
     B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
     if out is None:
         out = torch.empty_like(q)
+    _check(q, k, v, out, cu_seqlens)
     st = _stream(q.device, stream)
     if cu_seqlens is None:
         _call("sparse_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), B_, Hq, Hkv, N, d,
@@ -203,6 +276,7 @@ def dense_causal_attn_prefill(q, k, v, *, B=None, cu_seqlens=None, max_seqlen=No
     B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
     if out is None:
         out = torch.empty_like(q)
+    _check(q, k, v, out, cu_seqlens)
     st = _stream(q.device, stream)
     if cu_seqlens is None:
         _call("dense_causal_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), B_, Hq, Hkv,
@@ -218,10 +292,15 @@ def fused_supported_blocksparse(Hq, Hkv, gamma, block_q) -> bool:
     return bool(load_library().da_fused_supported_blocksparse(Hq, Hkv, gamma, block_q))
 
 
-def _blocks(block_ptr, block_idx):
-    for name, t in (("block_ptr", block_ptr), ("block_idx", block_idx)):
-        if t.dtype != torch.int32 or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous int32 tensor")
+def _blocks(block_ptr, block_idx, B, Hkv, N, block_q):
+    """Pointers of the key-block lists after checking their device, dtype and
+    that block_ptr holds [B, Hkv, ceil(N / block_q) + 1] offsets."""
+    if block_q not in (64, 128, 256):
+        raise ValueError("block_q must be 64, 128 or 256")
+    nqb = -(-N // block_q)
+    if block_ptr.numel() != B * Hkv * (nqb + 1):
+        raise ValueError(f"block_ptr must hold B * Hkv * (ceil(N / block_q) + 1) = "
+                         f"{B * Hkv * (nqb + 1)} offsets (got {block_ptr.numel()})")
     return _ptr(block_ptr), _ptr(block_idx)
 
 
@@ -231,8 +310,9 @@ def blocksparse_attn_prefill(q, k, v, *, block_q, block_ptr, block_idx, B=None,
     B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
     if out is None:
         out = torch.empty_like(q)
+    _check(q, k, v, out, cu_seqlens, block_ptr=block_ptr, block_idx=block_idx)
     _call("blocksparse_attn_prefill", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(cu_seqlens),
-          B_, N, Hq, Hkv, d, block_q, *_blocks(block_ptr, block_idx),
+          B_, N, Hq, Hkv, d, block_q, *_blocks(block_ptr, block_idx, B_, Hkv, N, block_q),
           _stream(q.device, stream))
     return out
 
@@ -247,9 +327,11 @@ def delta_attn_prefill_blocksparse(q, k, v, *, block_q, block_ptr, block_idx, ga
     nbytes = workspace_bytes(B_, N, Hq, Hkv, d, gamma)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+    _check(q, k, v, out, cu_seqlens, workspace, block_ptr, block_idx)
     wsz = workspace.numel() * workspace.element_size()
     _call("delta_attn_prefill_blocksparse", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
-          _ptr(cu_seqlens), B_, N, Hq, Hkv, d, block_q, *_blocks(block_ptr, block_idx), gamma,
+          _ptr(cu_seqlens), B_, N, Hq, Hkv, d, block_q,
+          *_blocks(block_ptr, block_idx, B_, Hkv, N, block_q), gamma,
           _ptr(workspace), wsz, _stream(q.device, stream), steps)
     return out
 

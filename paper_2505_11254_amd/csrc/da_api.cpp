@@ -419,6 +419,30 @@ da_status delta_attn_prefill_blocksparse(const void* q, const void* k, const voi
   return da::run_delta(P, workspace, workspace_bytes, stream, steps, false);
 }
 
+da_status da_launch_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, int block_q,
+                         da_plan* plan) {
+  if (!plan) return DA_ERR_NULL;
+  if (B < 1 || max_seqlen < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return DA_ERR_SHAPE;
+  if (gamma < 1) return DA_ERR_PARAM;
+  if (block_q != 0 && block_q != 64 && block_q != 128 && block_q != 256) return DA_ERR_PARAM;
+  if (d != 64 && d != 128) return DA_ERR_UNSUPPORTED;
+  da::Plan p;
+  if (!da::make_plan(B, max_seqlen, Hq, Hkv, d, gamma, &p)) return DA_ERR_SHAPE;
+  const int G = Hq / Hkv;
+  const int hpw = da::heads_per_block(G);
+  if (block_q && da::kRowsPerWave * (da::kAttnWaves / hpw) > block_q) return DA_ERR_UNSUPPORTED;
+  const int fhpw = da::fused_heads_per_block(G, gamma, block_q ? block_q : INT32_MAX);
+  plan->fused = fhpw > 0 ? 1 : 0;
+  plan->sparse_heads = fhpw > 0 ? fhpw : hpw;
+  plan->rows_heads = hpw;
+  plan->key_chunks = p.nC;
+  plan->chunk_keys = p.chunk;
+  plan->key_tile = da::kKeyTile;
+  plan->rows_per_wave = da::kRowsPerWave;
+  plan->waves_per_block = da::kAttnWaves;
+  return DA_OK;
+}
+
 size_t da_workspace_bytes(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma) {
   da::Plan p;
   if (!da::make_plan(B, max_seqlen, Hq, Hkv, d, gamma, &p)) return 0;

@@ -354,8 +354,11 @@ void attn_kernel(Args a) {
 #pragma unroll
   for (int mb = 0; mb < D / 32; ++mb) o[mb] = f32x16{};
   // Reference `ref` of the base-2 logits (same in lanes l and l^32; has_ref: a
-  // reference exists) and -ref in every register of nref, the block the
-  // score accumulators start from, so they hold logit - ref.
+  // reference exists) and -ref / c in every register of nref, the block the
+  // score accumulators start from, so that c times them is logit - ref.
+  // (Scaling the queries by c ahead of the MFMA would round c q to bf16 once
+  // more, an error proportional to the logits themselves.)
+  const float qscale = a.scale_log2, inv_qscale = 1.f / a.scale_log2;
   float ref = 0.f;
   bool has_ref = false;
   f32x16 nref = f32x16{};
@@ -417,9 +420,11 @@ void attn_kernel(Args a) {
     }
   };
 
-  // Online-softmax update with one tile's scores s = logit - ref: adds the
-  // tile's weights to l and returns them as bf16 P^T fragments, moving the
-  // reference first when it has to.
+  // Online-softmax update with one tile's scores: the accumulators hold
+  // s = q.k - ref / c, so c s = logit - ref in base-2 units, with c =
+  // log2(e)/sqrt(d) applied in fp32 here (the queries stay as given); adds
+  // the tile's weights to l and returns them as bf16 P^T fragments, moving
+  // the reference first when it has to.
   //
   // The reference lags the true running max: weights are taken against the
   // current one, and only if some lane's share of the tile's weight sum exceeds
@@ -438,8 +443,8 @@ void attn_kernel(Args a) {
       f32x16 p0, p1;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        p0[i] = fast_exp2(s0[i]);
-        p1[i] = fast_exp2(s1[i]);
+        p0[i] = fast_exp2(qscale * s0[i]);
+        p1[i] = fast_exp2(qscale * s1[i]);
       }
       pf[0] = __builtin_convertvector(p0.lo, bf16x8);
       pf[1] = __builtin_convertvector(p0.hi, bf16x8);
@@ -453,16 +458,16 @@ void attn_kernel(Args a) {
         ta = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 4, 5), ones2, ta, false);
         tb = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf[f], pf[f], 6, 7), ones2, tb, false);
       }
-      // the exponentials go two at a time with two other VALU instructions
-      // (conversions, sums) between them: a wave issues one exponential
-      // every ~15 clocks and fits its other VALU work into those gaps
-      __builtin_amdgcn_sched_group_barrier(0x400, 4, 0);
+      // the exponentials go two at a time with other VALU instructions (the
+      // scaling multiplies, conversions, sums) between them: a wave issues one
+      // exponential every ~15 clocks and fits its other VALU work into those
+      // gaps
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
 #pragma unroll
-      for (int i = 0; i < 14; ++i) {
+      for (int i = 0; i < 16; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
       return ta + tb;
     };
     float t = INFINITY;
@@ -482,7 +487,7 @@ void attn_kernel(Args a) {
       {
         const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
                                                          false, false);
-        mx = fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));
+        mx = qscale * fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));  // base 2
       }
       // a lane without a reference takes its tile max (if it sees any key);
       // one with a reference moves only up
@@ -496,11 +501,12 @@ void attn_kernel(Args a) {
         l *= alpha;
 #pragma unroll
         for (int mb = 0; mb < D / 32; ++mb) o[mb] *= alpha;
+        const float dr = dm * inv_qscale;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          s0[i] -= dm;
-          s1[i] -= dm;
-          nref[i] = -ref;
+          s0[i] -= dr;
+          s1[i] -= dr;
+          nref[i] = -ref * inv_qscale;
         }
       }
       t = weights();
@@ -588,11 +594,6 @@ void attn_kernel(Args a) {
   if (dsrc) *(f32x4*)(dpre + tid * 4) = dreg;
   for (int u = tid + kAttnThreads; u < nvec; u += kAttnThreads)
     if (const f32x4* src = dense_src(u)) *(f32x4*)(dpre + u * 4) = *src;
-  // Queries pre-scaled by log2(e)/sqrt(d) and rounded to bf16 once, so the
-  // score accumulators hold base-2 logits and the weights need no multiply.
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk)
-    qf[kk] = __builtin_convertvector(__builtin_convertvector(qf[kk], f32x8) * a.scale_log2, bf16x8);
 
   // ---- main loop over a ring of NS LDS stages, one barrier per tile.  Step
   // `it` waits until this wave's DMA of tile it has landed (later tiles may

@@ -220,3 +220,18 @@ def test_check_inputs_validates_its_arguments(lib):
     assert f(None, 1, 128, 0, 64, FAKE, FAKE, 10, FAKE, None) == 2        # Hkv < 1
     assert f(None, 1, 128, 2, 64, FAKE, None, 10, FAKE, None) == 1        # entries without idx
     assert f(FAKE, 1, 128, 2, 64, None, None, 0, FAKE + 2, None) == 5     # result alignment
+
+
+def test_launch_plan_validates_and_answers_without_a_gpu(lib):
+    from paper_2505_11254_amd import binding
+    p = binding.Plan()
+    ok = (1, 1 << 20, 32, 8, 128, 64, 0)
+    assert lib.da_launch_plan(*ok, ctypes.byref(p)) == 0
+    assert (p.fused, p.sparse_heads, p.rows_heads, p.key_chunks, p.chunk_keys) == (1, 4, 4, 16, 65536)
+    assert lib.da_launch_plan(*ok, None) == 1                                   # DA_ERR_NULL
+    for args, status in [((0, 1024, 4, 2, 64, 8, 0), 2), ((1, 1024, 4, 3, 64, 8, 0), 2),
+                         ((1, 1024, 4, 2, 64, 0, 0), 3), ((1, 1024, 4, 2, 64, 8, 32), 3),
+                         ((1, 1024, 4, 2, 96, 8, 0), 4),
+                         # a 64-row query block cannot hold one head's 128-row slab (G = 2)
+                         ((1, 1024, 4, 2, 64, 8, 64), 4)]:
+        assert lib.da_launch_plan(*args, ctypes.byref(p)) == status, args

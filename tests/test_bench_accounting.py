@@ -15,9 +15,8 @@ import bench  # noqa: E402
 from paper_2505_11254_amd.workloads import WORKLOADS, Workload  # noqa: E402
 
 
-def walk(wl, kind, hpw):
+def walk(wl, kind, hpw, chunk):
     ppw = 8 // hpw
-    chunk = bench.plan_chunk(wl)
     tot = 0
     for L in wl.seqlens:
         nA = L // wl.gamma
@@ -77,10 +76,34 @@ CASES = [
 @pytest.mark.parametrize("wl", CASES, ids=lambda w: w.name)
 @pytest.mark.parametrize("kind", ["sparse", "dense_rows", "dense"])
 def test_executed_pairs_match_tile_walk(wl, kind):
+    """The closed form equals the walk for every head grouping the kernels
+    can take, with the library's own key chunks."""
+    plan = bench.launch_plan(wl)
     G = wl.Hq // wl.Hkv
     for hpw in (1, 2, 4, 8):
         if G % hpw == 0:
-            assert bench.executed_pairs(wl, kind, hpw) == walk(wl, kind, hpw)
+            p = dict(plan, sparse_heads=hpw, rows_heads=hpw)
+            assert bench.executed_pairs(wl, kind, p) == walk(wl, kind, hpw, plan["chunk_keys"])
+
+
+def test_library_plan_of_the_workloads():
+    """The plan the library reports for the five workloads (da_launch_plan):
+    the tiling the kernels run and the counts above depend on."""
+    want = {  # fused, sparse heads, strided-row heads, key chunks, keys per chunk
+        "tiny_n1024_d64": (1, 1, 1, 1, 1024),
+        "llama8b_layer_32k": (1, 4, 4, 16, 2048),
+        "llama8b_layer_131k": (1, 4, 4, 16, 8192),
+        "llama8b_layer_1m": (1, 4, 4, 16, 65536),
+        "ragged_b4_gqa8": (1, 8, 8, 15, 8768),  # 16 chunks would pass the 8 GiB of partials
+    }
+    for name, w in want.items():
+        p = bench.launch_plan(WORKLOADS[name])
+        assert (p["fused"], p["sparse_heads"], p["rows_heads"], p["key_chunks"],
+                p["chunk_keys"]) == w, name
+        assert (p["key_tile"], p["rows_per_wave"], p["waves_per_block"]) == (64, 32, 8)
+    # gamma 48 with G = 2: no power-of-two head count makes a slab a multiple of 48
+    p = bench.launch_plan(Workload("x", (4096,), 4, 2, 128, 64, 4, 48, 0.0, 1))
+    assert p["fused"] == 0 and p["sparse_heads"] == p["rows_heads"] == 2
 
 
 def test_executed_covers_useful():
@@ -88,8 +111,7 @@ def test_executed_covers_useful():
     # where rows and windows are long against a tile
     for wl in WORKLOADS.values():
         sp, dr, dc = bench.pair_counts(wl.seqlens, wl.window, wl.n_sink, wl.gamma)
-        G = wl.Hq // wl.Hkv
-        es = bench.executed_pairs(wl, "sparse", bench.fused_heads_per_block(G, wl.gamma))
+        es = bench.executed_pairs(wl, "sparse")
         ed = bench.executed_pairs(wl, "dense_rows")
         ec = bench.executed_pairs(wl, "dense")
         assert es >= sp and ed >= dr and ec >= dc
