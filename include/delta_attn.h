@@ -249,6 +249,28 @@ da_status dense_causal_attn_prefill_varlen(const void* q, const void* k, const v
                                            void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the whole
+ * Delta path of delta_attn_prefill[_varlen] (cu_seqlens NULL: B sequences of
+ * max_seqlen tokens each), with its workspace in a static device array of
+ * DA_NOALLOC_SCRATCH_BYTES that every device the library runs on holds until
+ * the process ends.  The call allocates nothing.  The strided rows split
+ * their key axis into as many chunks as fit that array (fewer than
+ * delta_attn_prefill takes when its workspace would not fit), so the two
+ * calls can differ by rounding.  Returns DA_ERR_WORKSPACE when even one key
+ * chunk does not fit (for instance a single 1M-token sequence with 32 query
+ * heads); otherwise the statuses of delta_attn_prefill.  All calls on one
+ * device share its array, which keeps the last call's contents: calls that
+ * overlap on one device (other streams, other threads) race, so serialise
+ * them.
+ */
+#define DA_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+da_status delta_attn_prefill_noalloc(const void* q, const void* k, const void* v, void* out,
+                                     const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                     int Hkv, int d, int window, int n_sink, int gamma,
+                                     void* stream);
+
+/*
  * Workspace bytes delta_attn_prefill[_varlen] needs for these sizes
  * (max_seqlen = N for the fixed-length call).  0 if the sizes are invalid.
  */

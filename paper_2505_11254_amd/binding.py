@@ -35,6 +35,7 @@ SIGNATURES = {
     "blocksparse_attn_prefill": "pppppiiiiiippp",
     "delta_attn_prefill_blocksparse": "pppppiiiiiippipzpu",
     "da_check_inputs": "piiiipplpp",
+    "delta_attn_prefill_noalloc": "pppppiiiiiiiip",
 }
 
 
@@ -215,6 +216,20 @@ def delta_attn_prefill(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=Non
         _call("delta_attn_prefill_varlen", _ptr(q), _ptr(k), _ptr(v), _ptr(out),
               _ptr(cu_seqlens), B_, N, Hq, Hkv, d, window, n_sink, gamma, _ptr(workspace),
               wsz, st)
+    return out
+
+
+def delta_attn_prefill_noalloc(q, k, v, *, window, n_sink, gamma, B=None, cu_seqlens=None,
+                               max_seqlen=None, out=None, stream=None):
+    """Delta Attention prefill whose workspace is the library's static device
+    array (delta_attn_prefill_noalloc): the call allocates nothing on the
+    device; pass ``out`` to allocate nothing here either."""
+    B_, N, Hq, Hkv, d = _shapes(q, k, v, B, cu_seqlens, max_seqlen)
+    if out is None:
+        out = torch.empty_like(q)
+    _check(q, k, v, out, cu_seqlens)
+    _call("delta_attn_prefill_noalloc", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(cu_seqlens),
+          B_, N, Hq, Hkv, d, window, n_sink, gamma, _stream(q.device, stream))
     return out
 
 

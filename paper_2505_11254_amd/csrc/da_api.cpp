@@ -19,6 +19,7 @@ thread_local int g_last_hip_error = 0;
 // Per-device answer to "is this a gfx950": 0 unknown, 1 yes, 2 no.
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_arch_ok[kMaxDevices];
+thread_local int g_cur_dev = 0;  // the device check_device() last looked at
 
 da_status fail_hip(hipError_t e) {
   g_last_hip_error = (int)e;
@@ -38,6 +39,7 @@ da_status check_device() {
     st = (strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
     g_arch_ok[dev].store(st, std::memory_order_relaxed);
   }
+  g_cur_dev = dev;
   return st == 1 ? DA_OK : DA_ERR_UNSUPPORTED;
 }
 
@@ -66,8 +68,10 @@ int fused_heads_per_block(int G, int gamma, int max_rows) {
 // split into nC chunks of `chunk` keys (at least 2048), up to 16 of them.
 // Workgroups that run at the same time then process one key chunk each in
 // step with their neighbours, which keeps them sharing that chunk's keys and
-// values in L2.  nC drops only when the partial results would pass 8 GiB.
-bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p) {
+// values in L2.  nC drops only when the partial results would pass 8 GiB, or,
+// with a nonzero `limit`, until the whole workspace fits `limit` bytes
+// (false when even one chunk does not).
+bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p, size_t limit) {
   if (B < 1 || max_seqlen < 1 || Hq < 1 || Hkv < 1 || gamma < 1 || (d != 64 && d != 128))
     return false;
   if (Hq % Hkv != 0) return false;
@@ -79,19 +83,23 @@ bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p
   const int64_t per_chunk_bytes = (int64_t)B * Hq * nR_max * (d + 2) * 4;
   const int64_t budget = (int64_t)8 << 30;
   while (nC > 1 && per_chunk_bytes * nC > budget) --nC;
-  int64_t chunk = (max_seqlen + nC - 1) / nC;
-  chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
-  nC = (max_seqlen + chunk - 1) / chunk;
-  p->nA_max = (int)nA_max;
-  p->nR_max = (int)nR_max;
-  p->nC = (int)nC;
-  p->chunk = (int)chunk;
-  p->sa_floats = (size_t)B * Hq * nR_max * d;  // sparse anchor rows, or merged dense rows
-  p->part_o_floats = (size_t)B * Hq * nR_max * nC * d;
-  p->part_ml_floats = (size_t)B * Hq * nR_max * nC * 2;
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
-  p->bytes = up(p->sa_floats * 4) + up(p->part_o_floats * 4) + up(p->part_ml_floats * 4);
-  return true;
+  auto fill = [&](int64_t want) {
+    int64_t chunk = (max_seqlen + want - 1) / want;
+    chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
+    const int64_t n = (max_seqlen + chunk - 1) / chunk;
+    p->nA_max = (int)nA_max;
+    p->nR_max = (int)nR_max;
+    p->nC = (int)n;
+    p->chunk = (int)chunk;
+    p->sa_floats = (size_t)B * Hq * nR_max * d;  // sparse anchor rows, or merged dense rows
+    p->part_o_floats = (size_t)B * Hq * nR_max * n * d;
+    p->part_ml_floats = (size_t)B * Hq * nR_max * n * 2;
+    p->bytes = up(p->sa_floats * 4) + up(p->part_o_floats * 4) + up(p->part_ml_floats * 4);
+  };
+  fill(nC);
+  while (limit && p->bytes > limit && p->nC > 1) fill(p->nC - 1);
+  return !limit || p->bytes <= limit;
 }
 
 size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mode) {
@@ -202,7 +210,7 @@ da_status run_plain(const Problem& P, bool sparse, void* stream) {
 // schedule; `auto_fuse` lets the whole-path calls take the fused one.
 da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, void* stream,
                     unsigned steps, bool auto_fuse, int corr_mode = 0, float p0 = 0.f,
-                    float p1 = 0.f, float p2 = 0.f) {
+                    float p1 = 0.f, float p2 = 0.f, bool scratch = false) {
   da_status st = validate(P, true, true);
   if (st != DA_OK) return st;
   if ((steps & DA_STEP_ALL) == 0u || steps > (DA_STEP_ALL | DA_STEP_FUSED)) return DA_ERR_PARAM;
@@ -215,9 +223,15 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   const bool fused = (steps & DA_STEP_FUSED) || (auto_fuse && can_fuse);
   Plan plan;
   if (!make_plan(P.B, P.N, P.Hq, P.Hkv, P.d, P.gamma, &plan)) return DA_ERR_SHAPE;
-  const size_t extra = correction_floats(P.B, P.N, P.Hq, P.d, P.gamma, corr_mode) * 4;
-  if (!workspace || workspace_bytes < plan.bytes + extra) return DA_ERR_WORKSPACE;
-  if (!aligned16(workspace)) return DA_ERR_ALIGN;
+  if (scratch) {
+    // the static scratch array: as many key chunks as fit it
+    if (!make_plan(P.B, P.N, P.Hq, P.Hkv, P.d, P.gamma, &plan, kScratchBytes))
+      return DA_ERR_WORKSPACE;
+  } else {
+    const size_t extra = correction_floats(P.B, P.N, P.Hq, P.d, P.gamma, corr_mode) * 4;
+    if (!workspace || workspace_bytes < plan.bytes + extra) return DA_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return DA_ERR_ALIGN;
+  }
   {
     const int hpw = heads_per_block(P.Hq / P.Hkv);
     const int64_t rows_per_block = (int64_t)kRowsPerWave * (kAttnWaves / hpw);
@@ -233,6 +247,12 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   }
   st = check_device();
   if (st != DA_OK) return st;
+  if (scratch) {
+    // this device's copy of the static array (its address is looked up once
+    // per device, with the device current)
+    const hipError_t e = scratch_address(g_cur_dev, &workspace);
+    if (e != hipSuccess) return fail_hip(e);
+  }
 
   Args a = base_args(P);
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
@@ -341,6 +361,14 @@ da_status delta_attn_prefill_correction(const void* q, const void* k, const void
   Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
   return da::run_delta(P, workspace, workspace_bytes, stream, DA_STEP_ALL, true, mode, p0, p1,
                        p2);
+}
+
+da_status delta_attn_prefill_noalloc(const void* q, const void* k, const void* v, void* out,
+                                     const int32_t* cu_seqlens, int B, int max_seqlen, int Hq,
+                                     int Hkv, int d, int window, int n_sink, int gamma,
+                                     void* stream) {
+  Problem P{q, k, v, out, cu_seqlens, B, max_seqlen, Hq, Hkv, d, window, n_sink, gamma};
+  return da::run_delta(P, nullptr, 0, stream, DA_STEP_ALL, true, 0, 0.f, 0.f, 0.f, true);
 }
 
 size_t da_workspace_bytes_correction(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma,

@@ -7,6 +7,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "delta_attn.h"
+
 namespace da {
 
 // Keys per tile of every attention kernel, and query rows per wavefront.
@@ -107,7 +109,15 @@ struct Plan {
   size_t bytes;
 };
 
-bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p);
+bool make_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, Plan* p,
+               size_t limit = 0);
+
+// The allocation-free entry point's workspace: a static device array of
+// kScratchBytes (da_kernels.hip).  scratch_address gives its address on
+// device `dev`, which must be the current device; it is looked up once per
+// device and kept.
+constexpr size_t kScratchBytes = DA_NOALLOC_SCRATCH_BYTES;
+hipError_t scratch_address(int dev, void** p);
 // Extra workspace floats the correction variants need beyond the plan.
 size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mode);
 int heads_per_block(int G);

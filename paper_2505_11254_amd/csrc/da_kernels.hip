@@ -29,6 +29,8 @@
 
 #include <math.h>
 
+#include <atomic>
+
 namespace da {
 namespace {
 
@@ -1061,7 +1063,30 @@ hipError_t launch_attn(const Args& a0, hipStream_t s, int64_t nblocks) {
   return hipGetLastError();
 }
 
+constexpr int kScratchDevices = 64;
+std::atomic<void*> g_scratch[kScratchDevices];
+
 }  // namespace
+
+// Workspace of the allocation-free entry point: each device the library runs
+// on holds its own copy of this array until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is a stand-in,
+// not a device address): it uses the address hipGetSymbolAddress gives for
+// the current device.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t scratch_address(int dev, void** p) {
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  void* a = g_scratch[dev].load(std::memory_order_acquire);
+  if (!a) {
+    const hipError_t e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!a) return hipErrorInvalidSymbol;
+    g_scratch[dev].store(a, std::memory_order_release);
+  }
+  *p = a;
+  return hipSuccess;
+}
 
 hipError_t launch_check_inputs(const int32_t* cu, int B, int max_seqlen, const int32_t* bptr,
                               const int32_t* bidx, int64_t nnz, int Hkv, int nqb,

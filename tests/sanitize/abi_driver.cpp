@@ -20,6 +20,11 @@ hipError_t launch_dense(const Args&, hipStream_t) { ++g_launched; return hipSucc
 hipError_t launch_dense_rows(const Args&, hipStream_t) { ++g_launched; return hipSuccess; }
 hipError_t launch_delta_epilogue(const Args&, hipStream_t) { ++g_launched; return hipSuccess; }
 hipError_t launch_correction(const Args&, hipStream_t) { ++g_launched; return hipSuccess; }
+hipError_t scratch_address(int, void** p) {
+  ++g_launched;
+  *p = nullptr;
+  return hipSuccess;
+}
 hipError_t launch_check_inputs(const int32_t*, int, int, const int32_t*, const int32_t*, int64_t,
                                int, int, int32_t*, hipStream_t) {
   ++g_launched;

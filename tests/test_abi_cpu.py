@@ -235,3 +235,23 @@ def test_launch_plan_validates_and_answers_without_a_gpu(lib):
                          # a 64-row query block cannot hold one head's 128-row slab (G = 2)
                          ((1, 1024, 4, 2, 64, 8, 64), 4)]:
         assert lib.da_launch_plan(*args, ctypes.byref(p)) == status, args
+
+
+def test_noalloc_call_validates_and_bounds_its_scratch_before_the_gpu(lib):
+    """The allocation-free entry point rejects bad arguments like the others,
+    and a problem whose workspace cannot fit its static array (even with one
+    key chunk) with DA_ERR_WORKSPACE, all before any HIP call."""
+    def call(q=FAKE, out=FAKE, cu=None, B=1, N=1024, Hq=8, Hkv=2, d=128, w=64, s=4, g=16):
+        return lib.delta_attn_prefill_noalloc(q, FAKE, FAKE, out, cu, B, N, Hq, Hkv, d, w, s, g,
+                                              None)
+    assert call(q=None) == 1 and call(out=None) == 1
+    assert call(B=0) == 2 and call(Hq=6, Hkv=4) == 2
+    assert call(w=0) == 3 and call(g=0) == 3
+    assert call(d=96) == 4
+    assert call(q=FAKE + 8) == 5
+    # 1M tokens with 32 query heads: the merged rows alone need 269 MB > 256 MiB
+    assert call(N=1 << 20, Hq=32, Hkv=8, w=2048, s=64, g=64) == 6
+    # the whole plan of 131072 such tokens (596 MB) does not fit, but fewer key
+    # chunks do: that call passes this check (it then needs the GPU)
+    from paper_2505_11254_amd import binding
+    assert binding.workspace_bytes(1, 1 << 17, 32, 8, 128, 64) > 256 << 20
