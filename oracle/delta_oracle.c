@@ -400,7 +400,11 @@ static int delta_rows(const dao_problem* Pp, int smode, int gamma, const int64_t
     double* sp_i = (double*)malloc(sizeof(double) * (size_t)d);
     double* sp_a = (double*)malloc(sizeof(double) * (size_t)d);
     double* dn_a = (double*)malloc(sizeof(double) * (size_t)d);
-#pragma omp for schedule(dynamic, 1)
+    /* the anchor rows sp_a, dn_a last evaluated by this thread: rows listed
+     * group after group reuse them (the same values, evaluated once) */
+    int cb = -1, ch = -1;
+    int64_t ca = -1;
+#pragma omp for schedule(dynamic, 64)
     for (int64_t it = 0; it < n_rows; ++it) {
       if (!x || !sp_i || !sp_a || !dn_a) {
 #pragma omp atomic write
@@ -426,8 +430,13 @@ static int delta_rows(const dao_problem* Pp, int smode, int gamma, const int64_t
       }
       const int64_t a = (i / gamma) * gamma;
       attn_row(&P, smode, b, h, i, sp_i, NULL, NULL, NULL, x);   /* (A*V)_i */
-      attn_row(&P, smode, b, h, a, sp_a, NULL, NULL, NULL, x);   /* (A*V)_a */
-      attn_row(&P, DAO_MODE_DENSE, b, h, a, dn_a, NULL, NULL, NULL, x);    /* (A~V)_a */
+      if (b != cb || h != ch || a != ca) {
+        attn_row(&P, smode, b, h, a, sp_a, NULL, NULL, NULL, x);   /* (A*V)_a */
+        attn_row(&P, DAO_MODE_DENSE, b, h, a, dn_a, NULL, NULL, NULL, x);    /* (A~V)_a */
+        cb = b;
+        ch = h;
+        ca = a;
+      }
       for (int c = 0; c < d; ++c) {
         const double dl = dn_a[c] - sp_a[c];
         o[c] = sp_i[c] + dl;

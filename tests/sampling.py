@@ -34,6 +34,30 @@ def sample_rows(seqlens, Hq, window, n_sink, gamma, n_random=96, seed=0):
     return sorted(rows)
 
 
+def stratified_rows(seqlens, Hq, window, n_sink, gamma, n_random=64, seed=0):
+    """(b, h, i) triples, every query head and every row of whole groups of
+    gamma rows, per sequence: the first 4 groups, the groups around the first
+    anchor whose Delta is not zero (n_sink + window), the last 4 whole groups,
+    n_random seeded groups, and the dense tail rows.  A whole group of all
+    heads is a whole workgroup slab of the fused sparse kernel (the
+    workloads' slabs hold gamma rows of every head of a GQA group), so every
+    XCD's block range is covered.  Sorted by (b, h, i): the oracle evaluates
+    each group's anchor rows once."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for b, L in enumerate(seqlens):
+        nA = L // gamma
+        groups = set(range(min(4, nA))) | set(range(max(0, nA - 4), nA))
+        c = (n_sink + window) // gamma
+        groups |= {g for g in (c - 1, c, c + 1) if 0 <= g < nA}
+        if nA:
+            groups |= {int(g) for g in rng.integers(0, nA, n_random)}
+        pos = [g * gamma + j for g in sorted(groups) for j in range(gamma)]
+        pos += list(range(nA * gamma, L))
+        rows += [(b, h, i) for h in range(Hq) for i in pos]
+    return sorted(rows)
+
+
 def gather_rows(out: torch.Tensor, cu, rows) -> np.ndarray:
     """out[cu[b] + i, h] for every (b, h, i), as fp64 [n, d]."""
     cu = [int(x) for x in cu]

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from sampling import assert_parity, gather_rows, sample_rows, to_oracle_bits
+from sampling import assert_parity, gather_rows, sample_rows, stratified_rows, to_oracle_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -177,7 +177,10 @@ def test_stream_argument_orders_work_on_that_stream():
 
 # ---- workload-sized cases: sampled rows ----
 
-def _workload_case(name, check_plain=False):
+def _workload_case(name, check_plain=False, unfused=False):
+    """A workload on the stratified rows (every head, whole groups: the first
+    and last groups, those around the first corrected anchor, 64 seeded ones,
+    tail rows), checked exactly against the oracle's row entry points."""
     from paper_2505_11254_amd import WORKLOADS
     from paper_2505_11254_amd.inputs import generate
     wl = WORKLOADS[name]
@@ -186,17 +189,31 @@ def _workload_case(name, check_plain=False):
           else dict(B=wl.B))
     out = B().delta_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, gamma=wl.gamma,
                                  **kw)
-    sp = de = None
+    cun = wl.cu_seqlens()
+    rows = stratified_rows(wl.seqlens, wl.Hq, wl.window, wl.n_sink, wl.gamma, seed=len(name))
+    got = gather_rows(out, cun, rows)
+    got_u = got_sp = got_de = None
+    if unfused:  # the unfused schedule (sparse, strided rows, in-place epilogue)
+        ws = torch.empty(B().workspace_bytes(wl.B, wl.max_seqlen, wl.Hq, wl.Hkv, wl.d, wl.gamma),
+                         dtype=torch.uint8, device=DEV)
+        B().delta_attn_prefill_steps(q, k, v, out, ws, B().STEP_ALL, window=wl.window,
+                                     n_sink=wl.n_sink, gamma=wl.gamma,
+                                     cu_seqlens=None if wl.fixed_length else cu,
+                                     max_seqlen=wl.max_seqlen, B=wl.B)
+        got_u = gather_rows(out, cun, rows)
+        del ws
+    # the dense kernel on the boundary rows and seeded rows of sample_rows (a
+    # dense row costs the oracle up to the whole sequence)
+    drows = sample_rows(wl.seqlens, wl.Hq, wl.window, wl.n_sink, wl.gamma, seed=len(name))
     if check_plain:
         sp = B().sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, **kw)
+        got_sp = gather_rows(sp, cun, rows)
+        del sp
         de = B().dense_causal_attn_prefill(q, k, v, **kw)
+        got_de = gather_rows(de, cun, drows)
+        del de
     torch.cuda.synchronize()
-    cun = wl.cu_seqlens()
-    rows = sample_rows(wl.seqlens, wl.Hq, wl.window, wl.n_sink, wl.gamma, seed=len(name))
-    got = gather_rows(out, cun, rows)
-    got_sp = gather_rows(sp, cun, rows) if sp is not None else None
-    got_de = gather_rows(de, cun, rows) if de is not None else None
-    del out, sp, de
+    del out
     qb, kb, vb = (to_oracle_bits(x) for x in (q, k, v))
     del q, k, v
     torch.cuda.empty_cache()
@@ -204,13 +221,17 @@ def _workload_case(name, check_plain=False):
     ref = oracle.delta_attention_rows(qb, kb, vb, cu64, window=wl.window, n_sink=wl.n_sink,
                                       gamma=wl.gamma, rows=rows)
     err = assert_parity(got, ref, f"{name} delta path ({len(rows)} rows)")
-    print(f"{name}: delta path vs oracle on {len(rows)} rows: {err}", flush=True)
+    print(f"\n{name}: delta path vs oracle on {len(rows)} (row, head) pairs "
+          f"({len(rows) // wl.Hq} rows x {wl.Hq} heads): {err}", flush=True)
+    if got_u is not None:
+        err = assert_parity(got_u, ref, f"{name} unfused schedule ({len(rows)} rows)")
+        print(f"{name}: unfused schedule vs oracle on the same rows: {err}", flush=True)
     if got_sp is not None:
         ref_sp = oracle.attention(qb, kb, vb, cu64, mode=oracle.MODE_SPARSE, window=wl.window,
                                   n_sink=wl.n_sink, rows=rows)
-        assert_parity(got_sp, ref_sp, f"{name} sparse kernel")
-        ref_de = oracle.attention(qb, kb, vb, cu64, mode=oracle.MODE_DENSE, rows=rows)
-        assert_parity(got_de, ref_de, f"{name} dense kernel")
+        assert_parity(got_sp, ref_sp, f"{name} sparse kernel ({len(rows)} rows)")
+        ref_de = oracle.attention(qb, kb, vb, cu64, mode=oracle.MODE_DENSE, rows=drows)
+        assert_parity(got_de, ref_de, f"{name} dense kernel ({len(drows)} rows)")
 
 
 def test_workload_tiny_full_tensor():
@@ -225,23 +246,46 @@ def test_workload_tiny_full_tensor():
     assert_parity(out.cpu(), ref, "tiny workload")
 
 
-@pytest.mark.timeout(600)
-def test_workload_llama8b_32k_sampled():
-    _workload_case("llama8b_layer_32k", check_plain=True)
-
-
-@pytest.mark.timeout(600)
-def test_workload_llama8b_131k_sampled():
-    _workload_case("llama8b_layer_131k")
+@pytest.mark.timeout(900)
+def test_workload_llama8b_32k_full_tensor():
+    """The 32K layer in full: every element of the Delta output and of the
+    sparse kernel's output against the oracle (Algorithm 1 over the whole
+    sequence), the dense kernel on boundary and seeded rows."""
+    from paper_2505_11254_amd import WORKLOADS
+    from paper_2505_11254_amd.inputs import generate
+    wl = WORKLOADS["llama8b_layer_32k"]
+    q, k, v, cu = generate(wl, device=DEV)
+    out = B().delta_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink, gamma=wl.gamma)
+    sp = B().sparse_attn_prefill(q, k, v, window=wl.window, n_sink=wl.n_sink)
+    de = B().dense_causal_attn_prefill(q, k, v)
+    torch.cuda.synchronize()
+    rows = sample_rows(wl.seqlens, wl.Hq, wl.window, wl.n_sink, wl.gamma, seed=32)
+    got_de = gather_rows(de, wl.cu_seqlens(), rows)
+    out, sp = out.cpu(), sp.cpu()
+    qb, kb, vb = (to_oracle_bits(x) for x in (q, k, v))
+    del q, k, v, de
+    torch.cuda.empty_cache()
+    ref, ref_sp, _ = oracle.delta_attention(qb, kb, vb, None, window=wl.window, n_sink=wl.n_sink,
+                                            gamma=wl.gamma, return_parts=True)
+    err = assert_parity(out, ref, "32K delta path, whole tensor")
+    print(f"\n32K delta path vs oracle, all {ref.size} elements: {err}", flush=True)
+    assert_parity(sp, ref_sp, "32K sparse kernel, whole tensor")
+    ref_de = oracle.attention(qb, kb, vb, None, mode=oracle.MODE_DENSE, rows=rows)
+    assert_parity(got_de, ref_de, f"32K dense kernel ({len(rows)} rows)")
 
 
 @pytest.mark.timeout(900)
-def test_workload_ragged_b4_sampled():
+def test_workload_llama8b_131k_stratified():
+    _workload_case("llama8b_layer_131k", check_plain=True, unfused=True)
+
+
+@pytest.mark.timeout(900)
+def test_workload_ragged_b4_stratified():
     _workload_case("ragged_b4_gqa8")
 
 
 @pytest.mark.timeout(900)
-def test_workload_llama8b_1m_sampled():
+def test_workload_llama8b_1m_stratified():
     _workload_case("llama8b_layer_1m")
 
 

@@ -523,3 +523,18 @@ def test_planted_row_decode_mistake_fails_the_row_pins(name, tmp_path):
     mutated.write_text(text.replace(old, new))
     lib = oracle.build(force=True, src=str(mutated), dst=str(tmp_path / "libmutant.so"))
     assert not _row_pins_pass(oracle.Oracle(lib)), f"mutant {name} passed the row pins"
+
+
+def test_row_entry_point_is_order_independent():
+    """Rows of one group reuse its anchor rows inside the row entry point; the
+    result does not depend on how the rows are ordered or interleaved."""
+    seqlens = (300, 129)
+    (q, k, v), _, cu = rand_problem(seqlens, 4, 2, 16, seed=17, bf16=True)
+    full = oracle.delta_attention(q, k, v, cu, window=10, n_sink=3, gamma=16)
+    rows = [(b, h, i) for b, L in enumerate(seqlens) for h in range(4) for i in range(L)]
+    rng = np.random.default_rng(18)
+    for order in (np.arange(len(rows)), rng.permutation(len(rows))):
+        rr = [rows[n] for n in order]
+        got = oracle.delta_attention_rows(q, k, v, cu, window=10, n_sink=3, gamma=16, rows=rr)
+        for n, (b, h, i) in enumerate(rr):
+            assert np.array_equal(got[n], full[cu[b] + i, h])
