@@ -475,12 +475,9 @@ int dao_delta_attention_rows(const void* q, const void* k, const void* v, int in
  *                       successor and keeps Delta_i
  *   DAO_CORR_EMA        D = repeat(Delta, gamma); E_r = (1-b) E_{r-1} + b D_r
  *                       with E_{-1} = D_0, b = p0; c_r = E_r
- *   DAO_CORR_ABG        alpha-beta-gamma filter over the sequence Delta_0..:
- *                       o_0 = pos = Delta_0, vel = acc = 0; for i >= 1:
- *                       pred = pos + vel + acc/2, vpred = vel + acc,
- *                       res = Delta_i - pred, pos = pred + p0 res,
- *                       vel = vpred + p1 res, acc = acc + p2 res, o_i = pos;
- *                       c_r = o_{floor(r/gamma)}
+ *   DAO_CORR_ABG        alpha-beta-gamma filter over the sequence Delta_0..,
+ *                       in state-space form (see below): o_i is the filtered
+ *                       position after Delta_i; c_r = o_{floor(r/gamma)}
  * Rows past L_c take the dense result as in the other entry points.  Every
  * operation is elementwise over the d channels.
  */
@@ -531,19 +528,25 @@ int dao_delta_attention_variant(const void* q, const void* k, const void* v, int
           attn_row(&P, DAO_MODE_DENSE, b, h, i * gamma, cr, NULL, NULL, NULL, x);
           for (int c = 0; c < d; ++c) dl[i * d + c] = cr[c] - sp[i * gamma * d + c];
         }
-        /* alpha-beta-gamma filter: replace Delta_i by the filtered o_i */
+        /* The interpolation appendix's alpha-beta-gamma filter, as a
+         * state-space recursion over the anchors (unit step): state
+         * s = (position, velocity, acceleration), constant-acceleration
+         * transition F, the position observed, gain g = (p0, p1, p2):
+         *   predict s^ = F s,  residual e = Delta_i - s^_0,  update s = s^ + g e,
+         * from s = (Delta_0, 0, 0); Delta_i is replaced by the position. */
         if (mode == DAO_CORR_ABG && nA > 0) {
-          double *pos = st, *vel = st + d, *acc = st + 2 * d;
-          for (int c = 0; c < d; ++c) { pos[c] = dl[c]; vel[c] = 0.0; acc[c] = 0.0; }
+          static const double F[3][3] = {{1.0, 1.0, 0.5}, {0.0, 1.0, 1.0}, {0.0, 0.0, 1.0}};
+          const double g[3] = {p0, p1, p2};
+          double* sv = st; /* [3][d]: component r of channel c at sv[r * d + c] */
+          for (int c = 0; c < d; ++c) { sv[c] = dl[c]; sv[d + c] = 0.0; sv[2 * d + c] = 0.0; }
           for (int64_t i = 1; i < nA; ++i) {
             for (int c = 0; c < d; ++c) {
-              const double pred = pos[c] + vel[c] + 0.5 * acc[c];
-              const double vpred = vel[c] + acc[c];
-              const double res = dl[i * d + c] - pred;
-              pos[c] = pred + p0 * res;
-              vel[c] = vpred + p1 * res;
-              acc[c] = acc[c] + p2 * res;
-              dl[i * d + c] = pos[c];
+              double sh[3];
+              for (int r = 0; r < 3; ++r)
+                sh[r] = F[r][0] * sv[c] + F[r][1] * sv[d + c] + F[r][2] * sv[2 * d + c];
+              const double e = dl[i * d + c] - sh[0];
+              for (int r = 0; r < 3; ++r) sv[r * d + c] = sh[r] + g[r] * e;
+              dl[i * d + c] = sv[c];
             }
           }
         }

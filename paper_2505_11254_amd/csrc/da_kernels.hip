@@ -892,8 +892,9 @@ __global__ __launch_bounds__(kEpiThreads) void delta_epilogue_kernel(Args a) {
 //     entering the group, Ein_i, gives E_{a_i+k} = q^(k+1) Ein_i +
 //     (1 - q^(k+1)) Delta_i; the scan stores Ein_i and steps
 //     Ein_{i+1} = q^gamma Ein_i + (1 - q^gamma) Delta_i.
-//   alpha-beta-gamma filter (p0, p1, p2): position/velocity/acceleration
-//     update per anchor; Delta_i is replaced by the filtered position.
+//   alpha-beta-gamma filter (gain p0, p1, p2; the interpolation appendix's
+//     filter algorithm): a linear state-space recursion over the anchors;
+//     Delta_i is replaced by the filtered position.
 template <int CORR>
 __global__ __launch_bounds__(256) void corr_scan_kernel(Args a) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -926,20 +927,28 @@ __global__ __launch_bounds__(256) void corr_scan_kernel(Args a) {
       }
     }
   } else {
-    float pos = dl[0], vel = 0.f, acc = 0.f;
+    // The filter's state (position, velocity, acceleration) follows the
+    // linear recursion x_i = A x_{i-1} + g Delta_i, A = (I - g h) F: the
+    // constant-acceleration transition F (unit step) followed by the
+    // correction of the observed position (h = (1, 0, 0)) with gain g.
+    const float g0 = a.corr_p[0], g1 = a.corr_p[1], g2 = a.corr_p[2];
+    const float A[3][3] = {{1.f - g0, 1.f - g0, 0.5f * (1.f - g0)},
+                           {-g1, 1.f - g1, 1.f - 0.5f * g1},
+                           {-g2, -g2, 1.f - 0.5f * g2}};
+    float x0 = dl[0], x1 = 0.f, x2 = 0.f;
     for (int i0 = 1; i0 < nA; i0 += kB) {
 #pragma unroll
       for (int j = 0; j < kB; ++j) buf[j] = (i0 + j < nA) ? dl[(int64_t)(i0 + j) * a.d] : 0.f;
 #pragma unroll
       for (int j = 0; j < kB; ++j) {
         if (i0 + j < nA) {
-          const float pred = pos + vel + 0.5f * acc;
-          const float vpred = vel + acc;
-          const float res = buf[j] - pred;
-          pos = pred + a.corr_p[0] * res;
-          vel = vpred + a.corr_p[1] * res;
-          acc = acc + a.corr_p[2] * res;
-          dl[(int64_t)(i0 + j) * a.d] = pos;
+          const float y0 = A[0][0] * x0 + A[0][1] * x1 + A[0][2] * x2 + g0 * buf[j];
+          const float y1 = A[1][0] * x0 + A[1][1] * x1 + A[1][2] * x2 + g1 * buf[j];
+          const float y2 = A[2][0] * x0 + A[2][1] * x1 + A[2][2] * x2 + g2 * buf[j];
+          x0 = y0;
+          x1 = y1;
+          x2 = y2;
+          dl[(int64_t)(i0 + j) * a.d] = x0;
         }
       }
     }

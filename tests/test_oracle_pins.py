@@ -397,8 +397,10 @@ VARIANT_MUTANTS = {
     # so Delta_0 = D_0 = 0 exactly and both starts agree)
     "ema_weights_swapped": ("ema[c] = (1.0 - p0) * ema[c] + p0 * dl[i * d + c];",
                             "ema[c] = p0 * ema[c] + (1.0 - p0) * dl[i * d + c];"),
-    "abg_half_acc_dropped": ("const double pred = pos[c] + vel[c] + 0.5 * acc[c];",
-                             "const double pred = pos[c] + vel[c];"),
+    "abg_half_acc_dropped": ("{{1.0, 1.0, 0.5}, {0.0, 1.0, 1.0}, {0.0, 0.0, 1.0}}",
+                             "{{1.0, 1.0, 0.0}, {0.0, 1.0, 1.0}, {0.0, 0.0, 1.0}}"),
+    "abg_velocity_gain_on_acceleration": ("const double g[3] = {p0, p1, p2};",
+                                          "const double g[3] = {p0, p2, p1};"),
     "recompute_applied_everywhere": ("corr = (kk == 0) ? dl[i * d + c] : 0.0;",
                                      "corr = dl[i * d + c];"),
 }
