@@ -642,29 +642,30 @@ void attn_kernel(Args a) {
   // ---- epilogue: output register r of block mb is dim 32*mb + 8*(r/4) + 4*half + r%4
   const float lt = l + __shfl_xor(l, 32);
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-  if (MODE == kSparse && a.fuse) {
-    // Fused Delta store (the dense rows were merged into a.dense beforehand).
-    // Every group of gamma rows lies inside one head's row slab of this block,
-    // so its anchor's sparse row is in a register of some lane here: the
-    // anchor lane forms Delta = dense - sparse in fp32 over the dense row the
-    // prologue staged in LDS and leaves it there for the group's other rows,
-    // which store bf16(sparse + Delta), one rounding.  Anchor rows store the
-    // dense row, tail rows (past the last whole group) the dense row too;
-    // groups whose anchor lies below a.cover (a < n_sink + window: its sparse
-    // key set is all of [0, a]) have Delta = 0 exactly and keep the sparse row
-    // untouched.  Recompute (fuse 2) replaces anchors only.
+  if (MODE == kSparse) {
     const float inv = 1.f / lt;
-    const bool in_c = row_valid && my_pos < Lc;
-    // group of the row inside the block's slab (R0 is a multiple of gamma)
-    const int grp = in_c ? (int)fdiv((uint32_t)(my_pos - R0), a.fd_gamma) : 0;
-    const int anc = in_c ? R0 + grp * a.gamma : 0;
-    const bool open = in_c && (int64_t)anc >= a.cover;
-    const bool is_anchor = open && anc == my_pos;
-    const bool staged = a.gamma > 1;  // anchor dense rows are in dpre
-    const int xslot = ((wave & (a.hpw - 1)) * per_slab + grp) * D;
-    uint16_t* orow = a.out + ((sq.base + (row_valid ? my_pos : 0)) * a.Hq + h) * (int64_t)D;
-    if (a.fuse == 1 && staged) {
-      if (is_anchor) {
+    f32x4 val[D / 32][4];  // this lane's output row in fp32
+    if (a.fuse) {
+      // Fused Delta store (the dense rows were merged into a.dense beforehand).
+      // Every group of gamma rows lies inside one head's row slab of this
+      // block, so its anchor's sparse row is in a register of some lane here:
+      // the anchor lane forms Delta = dense - sparse in fp32 over the dense row
+      // the prologue staged in LDS and leaves it there for the group's other
+      // rows, which store bf16(sparse + Delta), one rounding.  Anchor rows
+      // store the dense row, tail rows (past the last whole group) the dense
+      // row too; groups whose anchor lies below a.cover (a < n_sink + window:
+      // its sparse key set is all of [0, a]) have Delta = 0 exactly and keep
+      // the sparse row untouched.  Recompute (fuse 2) replaces anchors only.
+      const bool in_c = row_valid && my_pos < Lc;
+      // group of the row inside the block's slab (R0 is a multiple of gamma)
+      const int grp = in_c ? (int)fdiv((uint32_t)(my_pos - R0), a.fd_gamma) : 0;
+      const int anc = in_c ? R0 + grp * a.gamma : 0;
+      const bool open = in_c && (int64_t)anc >= a.cover;
+      const bool is_anchor = open && anc == my_pos;
+      const bool staged = a.gamma > 1;  // anchor dense rows are in dpre
+      const bool delta = a.fuse == 1 && staged;
+      const int xslot = ((wave & (a.hpw - 1)) * per_slab + grp) * D;
+      if (delta && is_anchor) {
 #pragma unroll
         for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
@@ -674,41 +675,48 @@ void attn_kernel(Args a) {
                               o[mb][4 * jq + 2] * inv, o[mb][4 * jq + 3] * inv};
             const f32x4 dv = *(const f32x4*)(dpre + xslot + dim);
             *(f32x4*)(dpre + xslot + dim) = dv - sv;
-            *(bf16x4*)(orow + dim) = __builtin_convertvector(dv, bf16x4);
+            val[mb][jq] = dv;
           }
       }
-      __syncthreads();  // Delta of every group is in dpre
-      if (is_anchor) return;
-    }
-    if (!row_valid) return;
-    const bool tail = my_pos >= Lc;
-    const bool add = a.fuse == 1 && staged && open;
-    const float* gdrow =  // dense row in global memory: tail rows, and anchors when not staged
-        a.dense + (((int64_t)b * a.Hq + h) * a.nR_max + (in_c ? (int)fdiv((uint32_t)my_pos, a.fd_gamma)
-                                                                : nA + (my_pos - Lc))) * D;
-    // one branch per row kind (not one per vector): corrected rows fold the
-    // normalisation into the add, sparse rows only normalise, dense rows copy
-    f32x4 val[D / 32][4];
-    if (add) {
+      // Delta of every group is in dpre, and no wave reads the K/V ring any more
+      __syncthreads();
+      const bool tail = row_valid && my_pos >= Lc;
+      // one branch per row kind (not one per vector): corrected rows fold the
+      // normalisation into the add, sparse rows only normalise, dense rows copy
+      if (delta && is_anchor) {
+        // val holds the dense row
+      } else if (delta && open) {
 #pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb)
+        for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-        for (int jq = 0; jq < 4; ++jq) {
-          const f32x4 dl = *(const f32x4*)(dpre + xslot + 32 * mb + 8 * jq + 4 * half);
+          for (int jq = 0; jq < 4; ++jq) {
+            const f32x4 dl = *(const f32x4*)(dpre + xslot + 32 * mb + 8 * jq + 4 * half);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) val[mb][jq][e] = __builtin_fmaf(o[mb][4 * jq + e], inv, dl[e]);
-        }
-    } else if (tail || (is_anchor && !staged)) {
+            for (int e = 0; e < 4; ++e) val[mb][jq][e] = __builtin_fmaf(o[mb][4 * jq + e], inv, dl[e]);
+          }
+      } else if (tail || (is_anchor && !staged)) {
+        // dense row in global memory: tail rows, and anchors when not staged
+        const float* gdrow =
+            a.dense + (((int64_t)b * a.Hq + h) * a.nR_max +
+                       (in_c ? (int)fdiv((uint32_t)my_pos, a.fd_gamma) : nA + (my_pos - Lc))) * D;
 #pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb)
+        for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-        for (int jq = 0; jq < 4; ++jq) val[mb][jq] = *(const f32x4*)(gdrow + 32 * mb + 8 * jq + 4 * half);
-    } else if (is_anchor) {
+          for (int jq = 0; jq < 4; ++jq) val[mb][jq] = *(const f32x4*)(gdrow + 32 * mb + 8 * jq + 4 * half);
+      } else if (is_anchor) {
 #pragma unroll
-      for (int mb = 0; mb < D / 32; ++mb)
+        for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-        for (int jq = 0; jq < 4; ++jq)
-          val[mb][jq] = *(const f32x4*)(dpre + xslot + 32 * mb + 8 * jq + 4 * half);
+          for (int jq = 0; jq < 4; ++jq)
+            val[mb][jq] = *(const f32x4*)(dpre + xslot + 32 * mb + 8 * jq + 4 * half);
+      } else {
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+          for (int jq = 0; jq < 4; ++jq)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) val[mb][jq][e] = o[mb][4 * jq + e] * inv;
+      }
     } else {
 #pragma unroll
       for (int mb = 0; mb < D / 32; ++mb)
@@ -716,21 +724,49 @@ void attn_kernel(Args a) {
         for (int jq = 0; jq < 4; ++jq)
 #pragma unroll
           for (int e = 0; e < 4; ++e) val[mb][jq][e] = o[mb][4 * jq + e] * inv;
+      // the unfused schedule also keeps every anchor's sparse row in fp32
+      const int grp = (a.sa && row_valid) ? (int)fdiv((uint32_t)my_pos, a.fd_gamma) : 0;
+      if (a.sa && row_valid && grp * a.gamma == my_pos && my_pos < Lc) {
+        float* sarow = a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + grp) * D;
+#pragma unroll
+        for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+          for (int jq = 0; jq < 4; ++jq) *(f32x4*)(sarow + 32 * mb + 8 * jq + 4 * half) = val[mb][jq];
+      }
+      __syncthreads();  // no wave reads the K/V ring any more
     }
+    // The rows go out through LDS: each lane writes its row as bf16 into its
+    // wave's 32 x D region of the idle K/V ring (16-byte chunks XOR-swizzled
+    // by row), then every store instruction writes whole rows (64 lanes x 16
+    // bytes: four rows at d = 128) instead of 16 bytes of each of 32 rows
+    // that lie Hq * d elements apart.  The wave reads only what it wrote, and
+    // LDS runs a wave's instructions in order.
+    static_assert(NS * LD::stageElems >= kAttnWaves * kRowsPerWave * D, "output staging fits the ring");
+    constexpr int CPR = D / 8;     // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;  // rows per store instruction
+    uint16_t* const stg = smem + wave * (kRowsPerWave * D);
+    if (row_valid) {
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb)
+      for (int mb = 0; mb < D / 32; ++mb)
 #pragma unroll
-      for (int jq = 0; jq < 4; ++jq)
-        *(bf16x4*)(orow + 32 * mb + 8 * jq + 4 * half) = __builtin_convertvector(val[mb][jq], bf16x4);
+        for (int jq = 0; jq < 4; ++jq)
+          *(bf16x4*)(stg + col * D + (((4 * mb + jq) ^ (col & (CPR - 1))) * 8) + 4 * half) =
+              __builtin_convertvector(val[mb][jq], bf16x4);
+    }
+    const int rsub = lane / CPR, cc = lane % CPR;
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave / RPI; ++i) {
+      const int rr = i * RPI + rsub;
+      const u32x4 w = *(const u32x4*)(stg + rr * D + ((cc ^ (rr & (CPR - 1))) * 8));
+      const int r = wr0 + rr;
+      if (r < R1) *(u32x4*)(a.out + ((sq.base + r) * a.Hq + h) * (int64_t)D + cc * 8) = w;
+    }
     return;
   }
   if (!row_valid) return;
-  if (MODE != kDenseRows) {
+  if (MODE == kDense) {
     const float inv = 1.f / lt;
     uint16_t* orow = a.out + ((sq.base + my_pos) * a.Hq + h) * (int64_t)D;
-    const int grp = (MODE == kSparse && a.sa) ? (int)fdiv((uint32_t)my_pos, a.fd_gamma) : 0;
-    const bool write_sa = (MODE == kSparse) && a.sa && grp * a.gamma == my_pos && my_pos < Lc;
-    float* sarow = write_sa ? a.sa + (((int64_t)b * a.Hq + h) * a.nA_max + grp) * D : nullptr;
 #pragma unroll
     for (int mb = 0; mb < D / 32; ++mb) {
 #pragma unroll
@@ -739,7 +775,6 @@ void attn_kernel(Args a) {
         f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
                      o[mb][4 * jq + 3] * inv};
         *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
-        if (write_sa) *(f32x4*)(sarow + dim) = val;
       }
     }
   } else {
