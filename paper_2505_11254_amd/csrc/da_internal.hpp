@@ -78,6 +78,13 @@ struct Args {
   // the launch's divisors: row tiles, key chunks, sequences, GQA group size
   // Hq / Hkv, gamma, query block
   FastDiv fd_rtiles, fd_nC, fd_B, fd_G, fd_gamma, fd_bq;
+  // Dense-row workgroup order when every sequence has the same length (set by
+  // launch_dense_rows; dr_n1 = 0 keeps the plain order).  Row tiles
+  // [dr_t[c], dr_nrt) take the whole of key chunk c, [dr_z[c], dr_t[c]) part
+  // of it, lower ones none.  The dr_n1 whole-chunk (row tile, chunk) pairs run
+  // first, chunk by chunk, then the dr_n2 partial ones.
+  int dr_n1, dr_n2, dr_nrt;
+  int dr_t[16], dr_z[16];
 
   // Workspace of the Delta path (nullptr for the plain attention calls).
   float* sa;          // [B][Hq][nA_max][d]      sparse output at anchor rows, fp32

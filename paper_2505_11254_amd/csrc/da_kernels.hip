@@ -29,6 +29,7 @@
 
 #include <math.h>
 
+#include <algorithm>
 #include <atomic>
 
 namespace da {
@@ -186,7 +187,28 @@ void attn_kernel(Args a) {
   // Longest rows first: in the dense modes blocks dispatched together then have
   // (nearly) the same number of key tiles, start on the same tile and stay in
   // step, so they share each key/value tile in L2.
-  if (MODE != kSparse) rt = a.n_rtiles - 1 - rt;
+  if (MODE == kDenseRows && a.dr_n1 > 0) {
+    // Sequences of one length: every (row tile, chunk) pair that takes a whole
+    // key chunk runs before any that takes part of one.  The whole-chunk
+    // blocks all run the same number of tiles, so the blocks on one XCD stay
+    // in step over a chunk's tiles from round to round of the dispatch (a
+    // shorter diagonal block in between would start its CU on the next chunk
+    // early and put it out of step with the others).
+    int j = c * a.n_rtiles + rt;
+    if (j < a.dr_n1) {
+      c = 0;
+      for (int f; c < a.nC - 1 && j >= (f = a.dr_nrt - a.dr_t[c]); ++c) j -= f;
+      rt = a.dr_nrt - 1 - j;
+    } else if ((j -= a.dr_n1) < a.dr_n2) {
+      c = 0;
+      for (int f; c < a.nC - 1 && j >= (f = a.dr_t[c] - a.dr_z[c]); ++c) j -= f;
+      rt = a.dr_t[c] - 1 - j;
+    } else {
+      return;  // no key of any chunk is visible to this pair (uniform over the block)
+    }
+  } else if (MODE != kSparse) {
+    rt = a.n_rtiles - 1 - rt;
+  }
 
   const Seq sq = seq_of(a, b);
   const int L = sq.L;
@@ -1148,7 +1170,39 @@ hipError_t launch_dense(const Args& a, hipStream_t s) {
   return launch_attn<kDense>(a, s, (int64_t)a.B * a.n_hgroups * a.n_rtiles);
 }
 
-hipError_t launch_dense_rows(const Args& a, hipStream_t s) {
+hipError_t launch_dense_rows(const Args& a0, hipStream_t s) {
+  Args a = a0;
+  a.dr_n1 = a.dr_n2 = 0;
+  if (!a.cu && a.nC >= 1 && a.nC <= 16 && a.gamma >= 1) {
+    // Sequences of a.N tokens: the key tiles row tile rt takes from chunk c,
+    // for the dense rows (anchors r * gamma, then the tail rows) as the kernel
+    // decodes them.
+    const int64_t nA = a.N / a.gamma, Lc = nA * a.gamma, n_rows = nA + (a.N - Lc);
+    const int rpb = kRowsPerWave * a.ppw;
+    const int nrt = (int)((n_rows + rpb - 1) / rpb);
+    auto end = [&](int rt) {  // one past the last row's position
+      const int64_t r = std::min<int64_t>((int64_t)(rt + 1) * rpb, n_rows) - 1;
+      return (r < nA ? r * a.gamma : Lc + (r - nA)) + 1;
+    };
+    auto tiles = [&](int rt, int c) -> int64_t {
+      const int64_t kc0 = (int64_t)c * a.chunk, e = end(rt);
+      if (kc0 >= e) return 0;
+      return (std::min<int64_t>(kc0 + a.chunk, e) + kKeyTile - 1) / kKeyTile - kc0 / kKeyTile;
+    };
+    a.dr_nrt = nrt;
+    for (int c = 0; c < a.nC; ++c) {
+      const int64_t full = nrt > 0 ? tiles(nrt - 1, c) : 0;
+      int t = nrt, z = nrt;
+      if (full > 0) {
+        for (t = nrt; t > 0 && tiles(t - 1, c) == full;) --t;
+        for (z = t; z > 0 && tiles(z - 1, c) > 0;) --z;
+      }
+      a.dr_t[c] = t;
+      a.dr_z[c] = z;
+      a.dr_n1 += nrt - t;
+      a.dr_n2 += t - z;
+    }
+  }
   return launch_attn<kDenseRows>(a, s, (int64_t)a.B * a.n_hgroups * a.nC * a.n_rtiles);
 }
 
