@@ -785,35 +785,56 @@ void attn_kernel(Args a) {
     }
     return;
   }
-  if (!row_valid) return;
-  if (MODE == kDense) {
-    const float inv = 1.f / lt;
-    uint16_t* orow = a.out + ((sq.base + my_pos) * a.Hq + h) * (int64_t)D;
+  if (MODE == kDenseRows) {
+    // Unnormalised partial rows of this key chunk, through the idle ring like
+    // the sparse rows: each lane writes its fp32 row into its wave's 16 x D
+    // region (16-byte chunks XOR-swizzled by row), two passes of 16 rows, so
+    // that every store instruction writes whole rows (two of 512 bytes at
+    // d = 128) instead of 32 bytes of each of 32 rows nC * D floats apart.
+    __syncthreads();  // no wave reads the K/V ring any more
+    static_assert(NS * LD::stageElems * 2 >= kAttnWaves * 16 * D * 4, "partial staging fits the ring");
+    constexpr int CPR = D / 4;     // 16-byte chunks per fp32 row
+    constexpr int RPI = 64 / CPR;  // rows per store instruction
+    float* const stg = (float*)smem + wave * (16 * D);
+    const int rsub = lane / CPR, cc = lane % CPR;
+    const int64_t row0 = ((int64_t)b * a.Hq + h) * a.nR_max;
 #pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) {
+    for (int pass = 0; pass < 2; ++pass) {
+      if (row_valid && (col >> 4) == pass) {
+        const int r16 = col & 15;
 #pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int dim = 32 * mb + 8 * jq + 4 * half;
-        f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
-                     o[mb][4 * jq + 3] * inv};
-        *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
+        for (int mb = 0; mb < D / 32; ++mb)
+#pragma unroll
+          for (int jq = 0; jq < 4; ++jq)
+            *(f32x4*)(stg + r16 * D + (((8 * mb + 2 * jq + half) ^ (r16 & (CPR - 1))) * 4)) =
+                f32x4{o[mb][4 * jq], o[mb][4 * jq + 1], o[mb][4 * jq + 2], o[mb][4 * jq + 3]};
+      }
+#pragma unroll
+      for (int i = 0; i < 16 / RPI; ++i) {
+        const int rr = i * RPI + rsub;
+        const f32x4 w = *(const f32x4*)(stg + rr * D + ((cc ^ (rr & (CPR - 1))) * 4));
+        const int r = wr0 + 16 * pass + rr;
+        if (r < R1) *(f32x4*)(a.part_o + ((row0 + r) * a.nC + c) * D + cc * 4) = w;
       }
     }
-  } else {
-    const int64_t slot = (((int64_t)b * a.Hq + h) * a.nR_max + my_r) * a.nC + c;
-    float* po = a.part_o + slot * D;
-#pragma unroll
-    for (int mb = 0; mb < D / 32; ++mb) {
-#pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int dim = 32 * mb + 8 * jq + 4 * half;
-        *(f32x4*)(po + dim) = f32x4{o[mb][4 * jq], o[mb][4 * jq + 1], o[mb][4 * jq + 2],
-                                    o[mb][4 * jq + 3]};
-      }
-    }
-    if (half == 0) {
+    if (row_valid && half == 0) {
+      const int64_t slot = (row0 + my_r) * a.nC + c;
       a.part_ml[slot * 2] = has_ref ? ref : -INFINITY;  // -inf when no key of the chunk is visible
       a.part_ml[slot * 2 + 1] = lt;
+    }
+    return;
+  }
+  if (!row_valid) return;
+  const float inv = 1.f / lt;
+  uint16_t* orow = a.out + ((sq.base + my_pos) * a.Hq + h) * (int64_t)D;
+#pragma unroll
+  for (int mb = 0; mb < D / 32; ++mb) {
+#pragma unroll
+    for (int jq = 0; jq < 4; ++jq) {
+      const int dim = 32 * mb + 8 * jq + 4 * half;
+      f32x4 val = {o[mb][4 * jq] * inv, o[mb][4 * jq + 1] * inv, o[mb][4 * jq + 2] * inv,
+                   o[mb][4 * jq + 3] * inv};
+      *(bf16x4*)(orow + dim) = __builtin_convertvector(val, bf16x4);
     }
   }
 }
