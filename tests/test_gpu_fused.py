@@ -30,6 +30,10 @@ CASES = [
     ((500,), 2, 1, 64, 16, 2, 2),                 # gamma 2, d 64: the largest LDS exchange
     ((700,), 1, 1, 128, 50, 3, 2),                # gamma 2, d 128: the largest LDS exchange
     ((0, 450, 0, 64), 8, 2, 128, 64, 8, 32),      # empty sequences inside a ragged batch
+    # equal lengths through the fixed-length call, several key chunks per dense
+    # row: the strided blocks run whole-chunk (row tile, chunk) pairs first
+    ((5000, 5000, 5000), 8, 2, 128, 256, 16, 16),  # 3 chunks of 1728 keys, 8 tail rows
+    ((4100, 4100), 4, 4, 64, 96, 4, 64),           # G 1, d 64: 3 chunks, 4 tail rows
 ]
 
 
@@ -61,7 +65,8 @@ def test_fused_schedule_matches_oracle_and_unfused(lib, case):
     assert lib.fused_supported(Hq, Hkv, gamma)
     q, k, v, cu = random_qkv(seqlens, Hq, Hkv, d, seed=31 + gamma + len(seqlens))
     qd, kd, vd, cud = (x.cuda() for x in (q, k, v, cu))
-    kw = (dict(cu_seqlens=cud, max_seqlen=max(seqlens)) if len(seqlens) > 1 else dict(B=1))
+    fixed = len(set(seqlens)) == 1
+    kw = dict(B=len(seqlens)) if fixed else dict(cu_seqlens=cud, max_seqlen=max(seqlens))
     fused = _run(lib, qd, kd, vd, kw, w, s, gamma, lib.STEP_ALL | lib.STEP_FUSED)
     unfused = _run(lib, qd, kd, vd, kw, w, s, gamma, lib.STEP_ALL)
     default = lib.delta_attn_prefill(qd, kd, vd, window=w, n_sink=s, gamma=gamma, **kw)
