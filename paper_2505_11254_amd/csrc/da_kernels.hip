@@ -584,15 +584,6 @@ void attn_kernel(Args a) {
   for (int p = 0; p < NS - 1; ++p)
     if (p < n_iter) dma(tile_at(p), p);
 
-  // Q fragments: lane holds dims kk*16 + half*8 .. +8 of its row, for every kk.
-  // Rows past the end of the block load row R1-1's query (a valid row) and are
-  // never written, so no load sits behind a branch.
-  {
-    const int pos_ld = row_valid ? my_pos : row_pos<MODE>(R1 - 1, nA, Lc, a.gamma);
-    const uint16_t* qp = a.q + ((sq.base + pos_ld) * a.Hq + h) * (int64_t)D + half * 8;
-#pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + kk * 16);
-  }
   // Fused store: the merged dense rows of the block's anchors whose Delta is
   // not zero (anchor slot = head in block * groups per slab + group in slab),
   // staged in LDS so the epilogue does not wait on memory.  Each thread's
@@ -608,6 +599,46 @@ void attn_kernel(Args a) {
     return (const f32x4*)(a.dense + (((int64_t)b * a.Hq + hh) * a.nR_max +
                                      (int)fdiv((uint32_t)apos, a.fd_gamma)) * D + dv * 4);
   };
+
+  // Q fragments: lane holds dims kk*16 + half*8 .. +8 of its row, for every kk.
+  // Rows past the end of the block load row R1-1's query (a valid row) and are
+  // never written, so no load sits behind a branch.
+  //
+  // The sparse kernel, whose blocks are short, fetches its queries by LDS DMA
+  // instead: whole rows (four per instruction at d = 128), each lane fetching
+  // the 16-byte chunk that lands, XOR-swizzled by row, at its place in LDS.
+  // The staging is free LDS: ring stage 1 (filled only after the first
+  // barrier) for waves 0-3, the upper half of the dense-row area for waves
+  // 4-7 (when the staged dense rows fit the lower half).  Each lane reads its
+  // fragments from there.  Read straight into the fragment layout, every load
+  // instruction fetched 32 bytes of each of 32 rows, and at every block's start
+  // those loads queued behind each other in the memory pipeline.
+  constexpr int QCPR = D / 8;  // 16-byte chunks per query row
+  const bool q_lds = MODE == kSparse && nvec * 4 <= 64 * D;
+  uint16_t* const qst = smem + (wave < 4 ? LD::stageElems + wave * (kRowsPerWave * D)
+                                         : NS * LD::stageElems + 128 * D + (wave - 4) * (kRowsPerWave * D));
+  if (q_lds) {
+    static_assert(NS == 2 && 4 * kRowsPerWave * D <= LD::stageElems, "query staging fits stage 1");
+    constexpr int RPI = 64 / QCPR;  // rows per DMA instruction
+    const int jl = lane / QCPR, pc = lane % QCPR;
+    const uint32_t row_bytes = (uint32_t)__builtin_amdgcn_readfirstlane(a.Hq * D * 2);
+    const uint16_t* q0 = a.q + ((sq.base + R0) * a.Hq + h) * (int64_t)D;
+    const uint64_t qa = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uintptr_t)q0) |
+                        (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)((uintptr_t)q0 >> 32)) << 32;
+    const i32x4 qr = {(int)(uint32_t)qa, (int)((uint32_t)(qa >> 32) & 0xffffu), (int)0xfffffff0u, 0x00020000};
+    const uint32_t qdst = smem_lds + (uint32_t)(qst - smem) * 2;
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave / RPI; ++i) {
+      const int j = i * RPI + jl;  // row of the wave
+      const int r = min(wr0 + j, R1 - 1);
+      dma16(qr, qdst + i * 1024, (r - R0) * (int)row_bytes + ((pc ^ (j & (QCPR - 1))) * 16));
+    }
+  } else {
+    const int pos_ld = row_valid ? my_pos : row_pos<MODE>(R1 - 1, nA, Lc, a.gamma);
+    const uint16_t* qp = a.q + ((sq.base + pos_ld) * a.Hq + h) * (int64_t)D + half * 8;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) qf[kk] = *(const bf16x8*)(qp + kk * 16);
+  }
   const f32x4* dsrc = tid < nvec ? dense_src(tid) : nullptr;
   f32x4 dreg = f32x4{};
   if (dsrc) dreg = *dsrc;
@@ -615,6 +646,14 @@ void attn_kernel(Args a) {
   // MFMAs read qf every iteration and must not wait behind the DMA issued in
   // it, and the first tile is in this wave's part of stage 0.
   __builtin_amdgcn_s_waitcnt(0x0F70);
+  if (q_lds) {
+    // this wave's query rows have landed in its staging
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+      qf[kk] = *(const bf16x8*)(qst + col * D + (((2 * kk + half) ^ (col & (QCPR - 1))) * 8));
+    // the fragments are in registers before the barrier after which stage 1 fills
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+  }
   if (dsrc) *(f32x4*)(dpre + tid * 4) = dreg;
   for (int u = tid + kAttnThreads; u < nvec; u += kAttnThreads)
     if (const f32x4* src = dense_src(u)) *(f32x4*)(dpre + u * 4) = *src;
