@@ -72,6 +72,9 @@ def executed_pairs(wl, kind, plan=None):
     assert (plan["key_tile"], plan["rows_per_wave"], plan["waves_per_block"]) == (64, 32, 8)
     hpw = plan["sparse_heads"] if kind == "sparse" else plan["rows_heads"]
     ppw = 8 // hpw
+    # rows per head of a workgroup: the sparse slab may stop short of its
+    # wavefronts' rows (a multiple of gamma for the fused store)
+    slab = plan.get("sparse_slab_rows", 32 * ppw) if kind == "sparse" else 32 * ppw
     chunk = plan["chunk_keys"]
     tot = 0
     for L in wl.seqlens:
@@ -86,12 +89,15 @@ def executed_pairs(wl, kind, plan=None):
             pos = np.arange(L, dtype=np.int64)
         if n_rows == 0:
             continue
-        nw = -(-n_rows // 32)
-        w = np.arange(nw, dtype=np.int64)
-        R0 = (w // ppw) * 32 * ppw
-        R1 = np.minimum(R0 + 32 * ppw, n_rows)
-        wlo = pos[32 * w]
-        whi = pos[np.minimum(32 * w + 31, n_rows - 1)]
+        nb = -(-n_rows // slab)
+        R0 = np.repeat(np.arange(nb, dtype=np.int64) * slab, ppw)
+        wr0 = R0 + 32 * np.tile(np.arange(ppw, dtype=np.int64), nb)
+        R1 = np.minimum(R0 + slab, n_rows)
+        keep = wr0 < R1  # wavefronts with rows
+        R0, R1, wr0 = R0[keep], R1[keep], wr0[keep]
+        nw = int(keep.sum())
+        wlo = pos[wr0]
+        whi = pos[np.minimum(wr0 + 31, R1 - 1)]
         blo, bhi = pos[R0], pos[R1 - 1]
         if kind == "dense":
             tot += int((whi // 64 + 1).sum()) * 64 * 32

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define DA_ABI_VERSION 1
+#define DA_ABI_VERSION 2
 
 typedef enum {
   DA_OK = 0,
@@ -124,11 +124,16 @@ da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, 
                                    unsigned steps);
 
 /*
- * 1 if the fused schedule serves these sizes, else 0: some power of two h
- * dividing Hq/Hkv, h <= 8, has 256/h (the rows per query head of one sparse
- * workgroup) a multiple of gamma.  The fused schedule swaps the in-place
- * correction pass over `out` for a merge of the dense rows before the
- * sparse kernel, which then stores the corrected rows itself.
+ * 1 if the fused schedule serves these sizes, else 0.  The fused schedule
+ * swaps the in-place correction pass over `out` for a merge of the dense rows
+ * before the sparse kernel, which then stores the corrected rows itself; every
+ * group of gamma rows must lie inside one query head's row slab of a sparse
+ * workgroup.  A workgroup holds h query heads (h a power of two dividing
+ * Hq/Hkv, h <= 8) with up to 256/h rows each.  Fused when 256/h is a multiple
+ * of gamma for some h, or else when the largest multiple of gamma not above
+ * 256/h leaves at most 1/8 of the slab's rows idle for some h (then the slab
+ * holds that many rows: for the largest h that idles at most 1/16 of them,
+ * else for the h that idles fewest).
  */
 int da_fused_supported(int Hq, int Hkv, int gamma);
 
@@ -319,6 +324,9 @@ typedef struct {
   int key_tile;         /* keys per tile */
   int rows_per_wave;    /* query rows per wavefront */
   int waves_per_block;  /* wavefronts per attention workgroup */
+  int sparse_slab_rows; /* rows per query head of a sparse workgroup in that schedule: a
+                           multiple of gamma when fused (at most waves_per_block / heads *
+                           rows_per_wave, the wavefronts past it idle) */
 } da_plan;
 
 da_status da_launch_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, int block_q,

@@ -43,7 +43,7 @@ class Plan(ctypes.Structure):
     """da_plan of include/delta_attn.h: how the library tiles a problem."""
     _fields_ = [(n, ctypes.c_int) for n in ("fused", "sparse_heads", "rows_heads", "key_chunks",
                                             "chunk_keys", "key_tile", "rows_per_wave",
-                                            "waves_per_block")]
+                                            "waves_per_block", "sparse_slab_rows")]
 
     def as_dict(self):
         return {n: int(getattr(self, n)) for n, _ in self._fields_}

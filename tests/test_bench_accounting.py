@@ -15,7 +15,7 @@ import bench  # noqa: E402
 from paper_2505_11254_amd.workloads import WORKLOADS, Workload  # noqa: E402
 
 
-def walk(wl, kind, hpw, chunk):
+def walk(wl, kind, hpw, chunk, slab=None):
     ppw = 8 // hpw
     tot = 0
     for L in wl.seqlens:
@@ -31,7 +31,7 @@ def walk(wl, kind, hpw, chunk):
 
             def pos(r):
                 return r
-        rpb = 32 * ppw
+        rpb = slab if (slab and kind == "sparse") else 32 * ppw
         for R0 in range(0, n_rows, rpb):
             R1 = min(R0 + rpb, n_rows)
             lo, hi = pos(R0), pos(R1 - 1)
@@ -82,8 +82,14 @@ def test_executed_pairs_match_tile_walk(wl, kind):
     G = wl.Hq // wl.Hkv
     for hpw in (1, 2, 4, 8):
         if G % hpw == 0:
-            p = dict(plan, sparse_heads=hpw, rows_heads=hpw)
+            p = dict(plan, sparse_heads=hpw, rows_heads=hpw, sparse_slab_rows=256 // hpw)
             assert bench.executed_pairs(wl, kind, p) == walk(wl, kind, hpw, plan["chunk_keys"])
+            # a sparse slab of whole groups below the full 256 / hpw rows
+            slab = (256 // hpw) // wl.gamma * wl.gamma
+            if kind == "sparse" and 0 < slab < 256 // hpw:
+                p = dict(p, sparse_slab_rows=slab)
+                assert bench.executed_pairs(wl, kind, p) == walk(wl, kind, hpw, plan["chunk_keys"],
+                                                                 slab)
 
 
 def test_library_plan_of_the_workloads():
@@ -101,9 +107,18 @@ def test_library_plan_of_the_workloads():
         assert (p["fused"], p["sparse_heads"], p["rows_heads"], p["key_chunks"],
                 p["chunk_keys"]) == w, name
         assert (p["key_tile"], p["rows_per_wave"], p["waves_per_block"]) == (64, 32, 8)
-    # gamma 48 with G = 2: no power-of-two head count makes a slab a multiple of 48
+        assert p["sparse_slab_rows"] == 256 // p["sparse_heads"], name
+    # gamma 48 with G = 2: no power-of-two head count makes a slab a multiple of
+    # 48; one head per workgroup with 240 of its 256 rows (1/16 idle) does
     p = bench.launch_plan(Workload("x", (4096,), 4, 2, 128, 64, 4, 48, 0.0, 1))
+    assert (p["fused"], p["sparse_heads"], p["rows_heads"], p["sparse_slab_rows"]) == (1, 1, 2, 240)
+    # gamma 100: 200 of 256 rows (and 100 of 128, 0 of 64) would idle over 1/8
+    p = bench.launch_plan(Workload("y", (4096,), 4, 2, 128, 64, 4, 100, 0.0, 1))
     assert p["fused"] == 0 and p["sparse_heads"] == p["rows_heads"] == 2
+    assert p["sparse_slab_rows"] == 128
+    # gamma 3 with G = 4: 63 of 64 rows per head, four heads per workgroup
+    p = bench.launch_plan(Workload("z", (4096,), 8, 2, 128, 64, 4, 3, 0.0, 1))
+    assert (p["fused"], p["sparse_heads"], p["sparse_slab_rows"]) == (1, 4, 63)
 
 
 def test_executed_covers_useful():
