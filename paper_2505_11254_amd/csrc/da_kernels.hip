@@ -119,28 +119,48 @@ typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 // 16 bytes per lane from a buffer into LDS at byte address lds + 16*lane (LDS
-// DMA; rsrc and lds are wave-uniform).  Written as asm so that the compiler
-// does not track the transfer: its wait-count pass would otherwise wait for
-// every DMA in flight before any LDS read it cannot prove disjoint from the
-// DMA's target (the V^T reads of the current tile, while the next tile's DMA
-// is in flight).  The main loop waits for each tile's DMA itself (vmcnt)
-// before the barrier that publishes the tile.  The host pass of the kernel
-// templates sees an empty body.
-__device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t lds, int voff) {
+// DMA; rsrc and lds are wave-uniform scalars).  Written as asm so that the
+// compiler does not track the transfer: its wait-count pass would otherwise
+// wait for every DMA in flight before any LDS read it cannot prove disjoint
+// from the DMA's target (the V^T reads of the current tile, while the next
+// tile's DMA is in flight).  The main loop waits for each tile's DMA itself
+// (vmcnt) before the barrier that publishes the tile.  The host pass of the
+// kernel templates sees empty bodies.
+//
+// The compiler inserts no wait states for an instruction inside asm, and the
+// hardware does not interlock two of the operands here: a VMEM instruction
+// that reads an SGPR written by a VALU instruction (v_readfirstlane, which
+// builds the descriptors) needs 5 wait states, and an LDS DMA needs 1 after M0
+// is written.  With fewer it can read the SGPR's previous value: a stale
+// record count makes the fetch return zeros past it.  So the descriptors and
+// the LDS base of a group of DMAs first pass through settle_sgprs (s_nop 4,
+// which hands them back as its own outputs: every use comes after it, and
+// only scalar arithmetic lies between), and each DMA then waits the one state
+// M0 needs.
+// (read from the first lane: the compiler cannot hand asm a vector copy)
+__device__ __forceinline__ i32x4 first_lane(i32x4 r) {
+  return {__builtin_amdgcn_readfirstlane(r[0]), __builtin_amdgcn_readfirstlane(r[1]),
+          __builtin_amdgcn_readfirstlane(r[2]), __builtin_amdgcn_readfirstlane(r[3])};
+}
+__device__ __forceinline__ void settle_sgprs(i32x4& r0, i32x4& r1, uint32_t& m) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  // the descriptor and M0 must be scalar registers: read them from the first
-  // lane so the compiler cannot hand the asm a vector copy
-  const i32x4 sr = {__builtin_amdgcn_readfirstlane(rsrc[0]), __builtin_amdgcn_readfirstlane(rsrc[1]),
-                    __builtin_amdgcn_readfirstlane(rsrc[2]), __builtin_amdgcn_readfirstlane(rsrc[3])};
-  const int m0v = __builtin_amdgcn_readfirstlane((int)lds);
-  // The compiler inserts no wait states for an instruction inside asm, and the
-  // hardware does not interlock two of the operands here: a VMEM instruction
-  // that reads an SGPR written by a VALU instruction (v_readfirstlane above,
-  // often the one right before) needs 5 wait states, and an LDS DMA needs 1
-  // after M0 is written.  With fewer it can read the SGPR's previous value: a
-  // stale record count makes the fetch return zeros past it.  s_nop 4 gives 5.
-  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-               :: "v"(voff), "s"(sr), "{m0}"(m0v) : "memory");
+  r0 = first_lane(r0);
+  r1 = first_lane(r1);
+  m = (uint32_t)__builtin_amdgcn_readfirstlane((int)m);
+  asm volatile("s_nop 4" : "+s"(r0), "+s"(r1), "+s"(m));
+#endif
+}
+__device__ __forceinline__ void settle_sgprs(i32x4& r0, uint32_t& m) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  r0 = first_lane(r0);
+  m = (uint32_t)__builtin_amdgcn_readfirstlane((int)m);
+  asm volatile("s_nop 4" : "+s"(r0), "+s"(m));
+#endif
+}
+__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t lds, int voff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :: "v"(voff), "s"(rsrc), "{m0}"(lds) : "memory");
 #endif
 }
 
@@ -329,9 +349,10 @@ void attn_kernel(Args a) {
     keys = keys > kKeyTile ? kKeyTile : keys;
     const uint32_t nrec = (uint32_t)keys * key_bytes;
     const uint64_t ka = kaddr0 + off, va = vaddr0 + off;
-    const i32x4 kr = {(int)(uint32_t)ka, (int)((uint32_t)(ka >> 32) & 0xffffu), (int)nrec, 0x00020000};
-    const i32x4 vr = {(int)(uint32_t)va, (int)((uint32_t)(va >> 32) & 0xffffu), (int)nrec, 0x00020000};
-    const uint32_t st0 = smem_lds + (uint32_t)(stage * LD::stageElems) * 2;
+    i32x4 kr = {(int)(uint32_t)ka, (int)((uint32_t)(ka >> 32) & 0xffffu), (int)nrec, 0x00020000};
+    i32x4 vr = {(int)(uint32_t)va, (int)((uint32_t)(va >> 32) & 0xffffu), (int)nrec, 0x00020000};
+    uint32_t st0 = smem_lds + (uint32_t)(stage * LD::stageElems) * 2;
+    settle_sgprs(kr, vr, st0);
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
       const uint32_t region = (uint32_t)((wave_s * RPW + i) * 512) * 2;  // bytes
@@ -668,8 +689,9 @@ void attn_kernel(Args a) {
     const uint16_t* q0 = a.q + ((sq.base + R0) * a.Hq + h) * (int64_t)D;
     const uint64_t qa = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uintptr_t)q0) |
                         (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)((uintptr_t)q0 >> 32)) << 32;
-    const i32x4 qr = {(int)(uint32_t)qa, (int)((uint32_t)(qa >> 32) & 0xffffu), (int)0xfffffff0u, 0x00020000};
-    const uint32_t qdst = smem_lds + (uint32_t)(qst - smem) * 2;
+    i32x4 qr = {(int)(uint32_t)qa, (int)((uint32_t)(qa >> 32) & 0xffffu), (int)0xfffffff0u, 0x00020000};
+    uint32_t qdst = smem_lds + (uint32_t)(qst - smem) * 2;
+    settle_sgprs(qr, qdst);
 #pragma unroll
     for (int i = 0; i < kRowsPerWave / RPI; ++i) {
       const int j = i * RPI + jl;  // row of the wave

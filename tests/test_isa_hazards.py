@@ -30,6 +30,8 @@ _SECOND_DST = re.compile(r"^v_(add|sub|subrev|addc|subb|subbrev)_co_|^v_div_scal
 
 def _sgprs(op: str) -> set:
     op = op.strip()
+    if op == "m0":
+        return {-1}
     m = _SREG.match(op)
     if m:
         return {int(m.group(1))}
@@ -65,7 +67,7 @@ def dma_hazards(asm_lines) -> list:
         if ins is None or not (ins[0].startswith("buffer_load") and "lds" in ins[1][-1].split()):
             continue
         ops = ins[1]
-        reads = _sgprs(ops[1]) | (_sgprs(ops[2].split()[0]) if len(ops) > 2 else set())
+        reads = {-1} | _sgprs(ops[1]) | (_sgprs(ops[2].split()[0]) if len(ops) > 2 else set())
         waits, j = 0, i - 1
         while waits < VMEM_SGPR_WAITS:
             if j < 0 or insts[j] is None:
@@ -77,7 +79,8 @@ def dma_hazards(asm_lines) -> list:
                 if _SECOND_DST.search(mn) and len(o) > 1:
                     dst |= _sgprs(o[1])
                 if dst & reads:
-                    bad.append((i, f"{mn} writes s{sorted(dst & reads)} {waits} wait states before"))
+                    names = ["m0" if r < 0 else f"s{r}" for r in sorted(dst & reads)]
+                    bad.append((i, f"{mn} writes {','.join(names)} {waits} wait states before"))
                     break
             if waits < M0_WAITS and o and o[0] == "m0":
                 bad.append((i, f"{mn} writes m0 right before"))
@@ -96,12 +99,14 @@ def test_checker_flags_the_hazard_and_passes_the_wait():
         s_nop 0
         buffer_load_dwordx4 v139, s[36:39], 0 offen lds
     """.splitlines()
-    assert [r for _, r in dma_hazards(stale)] == ["v_readfirstlane_b32 writes s[38] 1 wait states before"]
+    assert [r for _, r in dma_hazards(stale)] == ["v_readfirstlane_b32 writes s38 1 wait states before"]
     waited = stale[:4] + ["        s_nop 4"] + stale[5:]
     assert dma_hazards(waited) == []
     m0 = ["v_readfirstlane_b32 s38, v36", "s_nop 4", "s_mov_b32 m0, s67",
           "buffer_load_dwordx4 v1, s[36:39], 0 offen lds"]
     assert [r for _, r in dma_hazards(m0)] == ["s_mov_b32 writes m0 right before"]
+    vm0 = ["v_readfirstlane_b32 m0, v3", "s_nop 1", "buffer_load_dwordx4 v1, s[36:39], 0 offen lds"]
+    assert [r for _, r in dma_hazards(vm0)] == ["v_readfirstlane_b32 writes m0 2 wait states before"]
     label = ["s_nop 1", ".LBB0_3:", "buffer_load_dwordx4 v1, s[36:39], 0 offen lds"]
     assert len(dma_hazards(label)) == 1
     # a VALU write of an SGPR the load does not read is no hazard
