@@ -97,7 +97,7 @@ def test_library_plan_of_the_workloads():
     the tiling the kernels run and the counts above depend on."""
     want = {  # fused, sparse heads, strided-row heads, key chunks, keys per chunk
         "tiny_n1024_d64": (1, 1, 1, 1, 1024),
-        "llama8b_layer_32k": (1, 4, 4, 16, 2048),
+        "llama8b_layer_32k": (1, 4, 4, 13, 2560),
         "llama8b_layer_131k": (1, 4, 4, 16, 8192),
         "llama8b_layer_1m": (1, 4, 4, 16, 65536),
         "ragged_b4_gqa8": (1, 8, 8, 15, 8768),  # 16 chunks would pass the 8 GiB of partials
