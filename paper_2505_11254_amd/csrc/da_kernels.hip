@@ -110,6 +110,18 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// The lanes of a wavefront exchange data through LDS here and there (each
+// writes its own part, then reads what other lanes wrote).  The hardware runs
+// a wave's LDS instructions in order, but the compiler knows nothing of the
+// other lanes: without a fence it may move a read above another lane's write
+// (into the branch that made that write conditional, say).  This orders every
+// LDS access before it against every one after it, with all lanes present.
+__device__ __forceinline__ void wave_lds_exchange() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Lane mask of a wavefront's predicate.
 __device__ __forceinline__ uint64_t wave_ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
@@ -712,7 +724,9 @@ void attn_kernel(Args a) {
   // it, and the first tile is in this wave's part of stage 0.
   __builtin_amdgcn_s_waitcnt(0x0F70);
   if (q_lds) {
-    // this wave's query rows have landed in its staging
+    // this wave's query rows have landed in its staging (each lane reads
+    // chunks other lanes fetched)
+    wave_lds_exchange();
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk)
       qf[kk] = *(const bf16x8*)(qst + col * D + (((2 * kk + half) ^ (col & (QCPR - 1))) * 8));
@@ -865,8 +879,8 @@ void attn_kernel(Args a) {
     // wave's 32 x D region of the idle K/V ring (16-byte chunks XOR-swizzled
     // by row), then every store instruction writes whole rows (64 lanes x 16
     // bytes: four rows at d = 128) instead of 16 bytes of each of 32 rows
-    // that lie Hq * d elements apart.  The wave reads only what it wrote, and
-    // LDS runs a wave's instructions in order.
+    // that lie Hq * d elements apart.  The wave reads only what it wrote (its
+    // lanes exchange rows through wave_lds_exchange).
     static_assert(NS * LD::stageElems >= kAttnWaves * kRowsPerWave * D, "output staging fits the ring");
     constexpr int CPR = D / 8;     // 16-byte chunks per row
     constexpr int RPI = 64 / CPR;  // rows per store instruction
@@ -879,14 +893,22 @@ void attn_kernel(Args a) {
           *(bf16x4*)(stg + col * D + (((4 * mb + jq) ^ (col & (CPR - 1))) * 8) + 4 * half) =
               __builtin_convertvector(val[mb][jq], bf16x4);
     }
+    wave_lds_exchange();
+    // All the wave's reads first (one wait for them), then the stores: row
+    // wr0 + rr of the wave lies rr * Hq * D elements past row wr0.
     const int rsub = lane / CPR, cc = lane % CPR;
+    constexpr int NI = kRowsPerWave / RPI;
+    u32x4 w[NI];
 #pragma unroll
-    for (int i = 0; i < kRowsPerWave / RPI; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const int rr = i * RPI + rsub;
-      const u32x4 w = *(const u32x4*)(stg + rr * D + ((cc ^ (rr & (CPR - 1))) * 8));
-      const int r = wr0 + rr;
-      if (r < R1) *(u32x4*)(a.out + ((sq.base + r) * a.Hq + h) * (int64_t)D + cc * 8) = w;
+      w[i] = *(const u32x4*)(stg + rr * D + ((cc ^ (rr & (CPR - 1))) * 8));
     }
+    uint16_t* const orow = a.out + ((sq.base + wr0 + rsub) * a.Hq + h) * (int64_t)D + cc * 8;
+    const int64_t rstep = (int64_t)RPI * a.Hq * D;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      if (wr0 + i * RPI + rsub < R1) *(u32x4*)(orow + i * rstep) = w[i];
     return;
   }
   if (MODE == kDenseRows) {
@@ -904,6 +926,7 @@ void attn_kernel(Args a) {
     const int64_t row0 = ((int64_t)b * a.Hq + h) * a.nR_max;
 #pragma unroll
     for (int pass = 0; pass < 2; ++pass) {
+      if (pass) wave_lds_exchange();  // the first pass's reads are done
       if (row_valid && (col >> 4) == pass) {
         const int r16 = col & 15;
 #pragma unroll
@@ -913,13 +936,21 @@ void attn_kernel(Args a) {
             *(f32x4*)(stg + r16 * D + (((8 * mb + 2 * jq + half) ^ (r16 & (CPR - 1))) * 4)) =
                 f32x4{o[mb][4 * jq], o[mb][4 * jq + 1], o[mb][4 * jq + 2], o[mb][4 * jq + 3]};
       }
+      wave_lds_exchange();
+      // reads first, then the stores (row r lies r * nC * D floats past row 0)
+      constexpr int NI = 16 / RPI;
+      f32x4 w[NI];
 #pragma unroll
-      for (int i = 0; i < 16 / RPI; ++i) {
+      for (int i = 0; i < NI; ++i) {
         const int rr = i * RPI + rsub;
-        const f32x4 w = *(const f32x4*)(stg + rr * D + ((cc ^ (rr & (CPR - 1))) * 4));
-        const int r = wr0 + 16 * pass + rr;
-        if (r < R1) *(f32x4*)(a.part_o + ((row0 + r) * a.nC + c) * D + cc * 4) = w;
+        w[i] = *(const f32x4*)(stg + rr * D + ((cc ^ (rr & (CPR - 1))) * 4));
       }
+      const int rb = wr0 + 16 * pass + rsub;
+      float* const prow = a.part_o + ((row0 + rb) * a.nC + c) * D + cc * 4;
+      const int64_t rstep = (int64_t)RPI * a.nC * D;
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        if (rb + i * RPI < R1) *(f32x4*)(prow + i * rstep) = w[i];
     }
     if (row_valid && half == 0) {
       const int64_t slot = (row0 + my_r) * a.nC + c;
