@@ -149,7 +149,9 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 // which hands them back as its own outputs: every use comes after it, and
 // only scalar arithmetic lies between), and each DMA then waits the one state
 // M0 needs.
-// (read from the first lane: the compiler cannot hand asm a vector copy)
+
+// A descriptor as read from the first lane (wave-uniform values in scalar
+// registers: the compiler cannot hand an "s" asm operand a vector copy).
 __device__ __forceinline__ i32x4 first_lane(i32x4 r) {
   return {__builtin_amdgcn_readfirstlane(r[0]), __builtin_amdgcn_readfirstlane(r[1]),
           __builtin_amdgcn_readfirstlane(r[2]), __builtin_amdgcn_readfirstlane(r[3])};
