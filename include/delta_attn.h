@@ -223,7 +223,9 @@ da_status delta_attn_prefill_blocksparse(const void* q, const void* k, const voi
                                          void* stream, unsigned steps);
 
 /* As da_fused_supported, with the sparse workgroup's rows per head also
- * within one query block of block_q rows. */
+ * within one query block of block_q rows (which fixes them at 256/h, so only
+ * slabs of all 256/h rows qualify: gamma must divide 256/h for some h whose
+ * 256/h rows fit block_q; no shortened slab). */
 int da_fused_supported_blocksparse(int Hq, int Hkv, int gamma, int block_q);
 
 /* Workspace bytes delta_attn_prefill_correction needs (0 if the sizes or mode are invalid). */
