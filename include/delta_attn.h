@@ -124,16 +124,11 @@ da_status delta_attn_prefill_steps(const void* q, const void* k, const void* v, 
                                    unsigned steps);
 
 /*
- * 1 if the fused schedule serves these sizes, else 0.  The fused schedule
- * swaps the in-place correction pass over `out` for a merge of the dense rows
- * before the sparse kernel, which then stores the corrected rows itself; every
- * group of gamma rows must lie inside one query head's row slab of a sparse
- * workgroup.  A workgroup holds h query heads (h a power of two dividing
- * Hq/Hkv, h <= 8) with up to 256/h rows each.  Fused when 256/h is a multiple
- * of gamma for some h, or else when the largest multiple of gamma not above
- * 256/h leaves at most 1/8 of the slab's rows idle for some h (then the slab
- * holds that many rows: for the largest h that idles at most 1/16 of them,
- * else for the h that idles fewest).
+ * 1 if the fused schedule serves these sizes, else 0: some power of two h
+ * dividing Hq/Hkv, h <= 8, has 256/h (the rows per query head of one sparse
+ * workgroup) a multiple of gamma.  The fused schedule swaps the in-place
+ * correction pass over `out` for a merge of the dense rows before the
+ * sparse kernel, which then stores the corrected rows itself.
  */
 int da_fused_supported(int Hq, int Hkv, int gamma);
 
@@ -223,9 +218,7 @@ da_status delta_attn_prefill_blocksparse(const void* q, const void* k, const voi
                                          void* stream, unsigned steps);
 
 /* As da_fused_supported, with the sparse workgroup's rows per head also
- * within one query block of block_q rows (which fixes them at 256/h, so only
- * slabs of all 256/h rows qualify: gamma must divide 256/h for some h whose
- * 256/h rows fit block_q; no shortened slab). */
+ * within one query block of block_q rows (256/h <= block_q). */
 int da_fused_supported_blocksparse(int Hq, int Hkv, int gamma, int block_q);
 
 /* Workspace bytes delta_attn_prefill_correction needs (0 if the sizes or mode are invalid). */
@@ -326,9 +319,9 @@ typedef struct {
   int key_tile;         /* keys per tile */
   int rows_per_wave;    /* query rows per wavefront */
   int waves_per_block;  /* wavefronts per attention workgroup */
-  int sparse_slab_rows; /* rows per query head of a sparse workgroup in that schedule: a
-                           multiple of gamma when fused (at most waves_per_block / heads *
-                           rows_per_wave, the wavefronts past it idle) */
+  int sparse_slab_rows; /* rows per query head of a sparse workgroup in that schedule:
+                           waves_per_block / sparse_heads * rows_per_wave (a multiple of gamma
+                           when fused) */
 } da_plan;
 
 da_status da_launch_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamma, int block_q,

@@ -55,39 +55,10 @@ int heads_per_block(int G) {
   return h;
 }
 
-int fused_heads_per_block(int G, int gamma, int max_rows, int* slab) {
+int fused_heads_per_block(int G, int gamma, int max_rows) {
   for (int h = heads_per_block(G); h >= 1; h /= 2) {
-    const int full = kRowsPerWave * (kAttnWaves / h);
-    if (G % h == 0 && full % gamma == 0 && full <= max_rows) {
-      if (slab) *slab = full;
-      return h;
-    }
-  }
-  if (max_rows == INT32_MAX) {
-    // A slab of whole groups below the full one; the wavefronts past it idle.
-    // More heads per workgroup share each key/value tile and keep the block's
-    // key span short, so the largest head count that idles at most 1/16 of
-    // its rows wins; failing that, the one that idles least, up to 1/8.
-    int best = 0, best_slab = 0, best_idle = 0, best_full = 1;
-    for (int h = heads_per_block(G); h >= 1; h /= 2) {
-      const int full = kRowsPerWave * (kAttnWaves / h);
-      const int s = full / gamma * gamma;
-      if (G % h != 0 || s == 0) continue;
-      if ((full - s) * 16 <= full) {
-        if (slab) *slab = s;
-        return h;
-      }
-      if (!best || (int64_t)(full - s) * best_full < (int64_t)best_idle * full) {
-        best = h;
-        best_slab = s;
-        best_idle = full - s;
-        best_full = full;
-      }
-    }
-    if (best && best_idle * kAttnWaves <= best_full) {
-      if (slab) *slab = best_slab;
-      return best;
-    }
+    const int slab = kRowsPerWave * (kAttnWaves / h);
+    if (G % h == 0 && slab % gamma == 0 && slab <= max_rows) return h;
   }
   return 0;
 }
@@ -215,7 +186,6 @@ Args base_args(const Problem& P) {
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)P.d));
   a.hpw = heads_per_block(P.Hq / P.Hkv);
   a.ppw = kAttnWaves / a.hpw;
-  a.slab = kRowsPerWave * a.ppw;
   a.n_hgroups = P.Hq / a.hpw;
   const int rows_per_block = kRowsPerWave * a.ppw;
   a.n_rtiles = (P.N + rows_per_block - 1) / rows_per_block;
@@ -251,9 +221,7 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
   if (corr_mode < DA_CORR_DELTA || corr_mode > DA_CORR_ABG) return DA_ERR_PARAM;
   if (!std::isfinite(p0) || !std::isfinite(p1) || !std::isfinite(p2)) return DA_ERR_PARAM;
   if (corr_mode == DA_CORR_EMA && (p0 < 0.f || p0 > 1.f)) return DA_ERR_PARAM;
-  int fslab = 0;
-  const int fhpw = fused_heads_per_block(P.Hq / P.Hkv, P.gamma, P.blk_ptr ? P.block_q : INT32_MAX,
-                                         &fslab);
+  const int fhpw = fused_heads_per_block(P.Hq / P.Hkv, P.gamma, P.blk_ptr ? P.block_q : INT32_MAX);
   const bool can_fuse = fhpw > 0 && corr_mode <= DA_CORR_RECOMPUTE;
   if ((steps & DA_STEP_FUSED) && !can_fuse) return DA_ERR_UNSUPPORTED;
   const bool fused = (steps & DA_STEP_FUSED) || (auto_fuse && can_fuse);
@@ -276,7 +244,8 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
     if ((int64_t)P.B * plan.nR_max * ((P.Hq + 8192 / P.d - 1) / (8192 / P.d)) > INT32_MAX)
       return DA_ERR_SHAPE;
     if (fused) {
-      if ((int64_t)P.B * (P.Hq / fhpw) * ((P.N + fslab - 1) / fslab) > INT32_MAX)
+      const int64_t frows = (int64_t)kRowsPerWave * (kAttnWaves / fhpw);
+      if ((int64_t)P.B * (P.Hq / fhpw) * ((P.N + frows - 1) / frows) > INT32_MAX)
         return DA_ERR_SHAPE;
     }
   }
@@ -327,9 +296,8 @@ da_status run_delta(const Problem& P, void* workspace, size_t workspace_bytes, v
       Args as = a;
       as.hpw = fhpw;
       as.ppw = kAttnWaves / fhpw;
-      as.slab = fslab;
       as.n_hgroups = P.Hq / fhpw;
-      as.n_rtiles = (P.N + fslab - 1) / fslab;
+      as.n_rtiles = (P.N + kRowsPerWave * as.ppw - 1) / (kRowsPerWave * as.ppw);
       e = launch_sparse(as, s);
       if (e != hipSuccess) return fail_hip(e);
     }
@@ -495,11 +463,10 @@ da_status da_launch_plan(int B, int max_seqlen, int Hq, int Hkv, int d, int gamm
   const int G = Hq / Hkv;
   const int hpw = da::heads_per_block(G);
   if (block_q && da::kRowsPerWave * (da::kAttnWaves / hpw) > block_q) return DA_ERR_UNSUPPORTED;
-  int fslab = 0;
-  const int fhpw = da::fused_heads_per_block(G, gamma, block_q ? block_q : INT32_MAX, &fslab);
+  const int fhpw = da::fused_heads_per_block(G, gamma, block_q ? block_q : INT32_MAX);
   plan->fused = fhpw > 0 ? 1 : 0;
   plan->sparse_heads = fhpw > 0 ? fhpw : hpw;
-  plan->sparse_slab_rows = fhpw > 0 ? fslab : da::kRowsPerWave * (da::kAttnWaves / hpw);
+  plan->sparse_slab_rows = da::kRowsPerWave * (da::kAttnWaves / (fhpw > 0 ? fhpw : hpw));
   plan->rows_heads = hpw;
   plan->key_chunks = p.nC;
   plan->chunk_keys = p.chunk;

@@ -73,8 +73,6 @@ struct Args {
   // Workgroup tiling of (query heads x rows): hpw heads of one kv group, each
   // with ppw sub-tiles of 32 rows; hpw * ppw == kAttnWaves.
   int hpw, ppw;
-  int slab;           // rows per head of a sparse workgroup (32 * ppw unless the
-                      // fused store needs a multiple of gamma below that)
   int n_hgroups;      // Hq / hpw
   int n_rtiles;       // row tiles (of 32 * ppw rows) per (sequence, head group)
   // the launch's divisors: row tiles, key chunks, sequences, GQA group size
@@ -130,15 +128,10 @@ hipError_t scratch_address(int dev, void** p);
 // Extra workspace floats the correction variants need beyond the plan.
 size_t correction_floats(int B, int max_seqlen, int Hq, int d, int gamma, int mode);
 int heads_per_block(int G);
-// Heads per workgroup of the fused sparse kernel, 0 when the fused store
-// cannot serve gamma, and in *slab the rows per head of its workgroups: the
-// largest power of two hpw dividing G (at most kAttnWaves) whose row slab,
-// 32 * kAttnWaves / hpw rows, is a multiple of gamma and at most max_rows.
-// Without key-block lists (max_rows = INT32_MAX) and without such an hpw, the
-// slab may be the largest multiple of gamma below it: for the largest hpw that
-// leaves at most 1/16 of the rows idle, else for the hpw that leaves the
-// fewest idle, if at most 1/kAttnWaves of them.
-int fused_heads_per_block(int G, int gamma, int max_rows, int* slab = nullptr);
+// Heads per workgroup of the fused sparse kernel: the largest power of two
+// dividing G (at most kAttnWaves) whose per-head row slab, 32 * kAttnWaves /
+// hpw rows, is a multiple of gamma and at most max_rows; 0 when there is none.
+int fused_heads_per_block(int G, int gamma, int max_rows);
 
 // Kernel launchers (da_kernels.hip).  Each returns the hipError_t of the launch.
 hipError_t launch_sparse(const Args& a, hipStream_t s);

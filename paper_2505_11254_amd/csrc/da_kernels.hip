@@ -122,9 +122,6 @@ __device__ __forceinline__ void wave_lds_exchange() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Lane mask of a wavefront's predicate.
-__device__ __forceinline__ uint64_t wave_ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
-
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 
@@ -264,9 +261,7 @@ void attn_kernel(Args a) {
   const int Lc = nA * a.gamma;
   const int n_rows = (MODE == kDenseRows) ? nA + (L - Lc) : L;
 
-  // rows per head of the block: the sparse kernel's slab may stop short of
-  // its wavefronts' rows (a multiple of gamma for the fused store)
-  const int rows_per_block = MODE == kSparse ? a.slab : kRowsPerWave * a.ppw;
+  const int rows_per_block = kRowsPerWave * a.ppw;
   const int R0 = rt * rows_per_block;
   if (R0 >= n_rows) return;  // uniform over the block
   const int R1 = min(R0 + rows_per_block, n_rows);
@@ -497,24 +492,14 @@ void attn_kernel(Args a) {
   // the reference first when it has to.
   //
   // The reference lags the true running max: weights are taken against the
-  // current one, and only when a lane's share of the tile's weight sum exceeds
-  // 2^13 (or a row has no reference yet) does the wave take the row max of the
-  // tile and move references up to it, rescaling O and l, and take the weights
-  // again.  Every weight stays below 2^13 (harmless in fp32 and bf16): a lane
-  // whose share is at most 2^13 has no weight above it, and a row that moved
-  // has every weight at most 1.  The result is the same in real arithmetic
-  // whatever the reference, since numerator and normaliser share it; the
-  // common tile pays no max reduction and no subtraction.
-  //
-  // Which rows move differs by kernel.  In the dense kernels the wave decides:
-  // once any lane passes the bound, every row whose tile max lies above its
-  // reference moves.  In the sparse kernel each row decides on its own
-  // evidence (its pair of lanes passed the bound, or it has no reference),
-  // so a row's arithmetic depends on its own scores and tile order alone and
-  // any tiling of rows into wavefronts gives the same bits: the fused
-  // schedule's slabs of whole groups need not line up with the unfused
-  // schedule's.  (It costs the dense-rows kernel about 1% to decide per row.)
-  constexpr bool kRowLocal = MODE == kSparse;
+  // current one, and only if some lane's share of the tile's weight sum exceeds
+  // 2^13 (or some lane has no reference yet) does the wave take the row max
+  // of the tile.  ref then moves up by it when a score exceeds ref by more than 8
+  // (a weight above 2^8), rescaling O and l, and the weights are taken again.
+  // Every weight stays below 2^13 (harmless in fp32 and bf16): a lane whose
+  // scores all lie within 8 of ref sums at most 32 * 2^8 = 2^13.  The result is
+  // the same either way, since numerator and normaliser share the reference;
+  // the common tile pays no max reduction and no subtraction.
   auto softmax = [&](f32x16& s0, f32x16& s1, bf16x8* pf) {
     // P^T fragment t covers keys 16t..16t+15: registers 8*(t%2)..+7 of block
     // t/2.  The sum covers the bf16 weights the MFMA multiplies (dot2 with 1,1),
@@ -550,19 +535,9 @@ void attn_kernel(Args a) {
       }
       return ta + tb;
     };
-    float t;
-    uint64_t tm = 0;  // rows (lane pairs) that must move, sparse kernel
-    bool slow;
-    if constexpr (kRowLocal) {
-      t = weights();  // lanes without a reference take theirs again below
-      tm = wave_ballot(!has_ref || !(t <= 8192.f));
-      slow = tm != 0;
-    } else {
-      t = INFINITY;
-      if (!__any(!has_ref)) t = weights();
-      slow = __any(!(t <= 8192.f));
-    }
-    if (slow) {
+    float t = INFINITY;
+    if (!__any(!has_ref)) t = weights();
+    if (__any(!(t <= 8192.f))) {
       // row max over the 32 scores of this lane (a tree of 3-input max), then
       // across the lane pair l, l^32 that shares the row
       float t3[11];
@@ -579,24 +554,12 @@ void attn_kernel(Args a) {
                                                          false, false);
         mx = qscale * fmaxf(__uint_as_float(pr[0]), __uint_as_float(pr[1]));  // base 2
       }
-      // a row without a reference takes its tile max (if it sees any key)
+      // a lane without a reference takes its tile max (if it sees any key);
+      // one with a reference moves only up
       const bool seen = mx != -INFINITY;
-      bool grow;
-      float dm;
-      if constexpr (kRowLocal) {
-        // a row with one moves up by its tile max when its lane pair passed
-        // the bound (the max then lies above 8); the pair is joined through
-        // the wave's ballot, in scalar registers
-        const uint64_t tp = tm | (tm >> 32) | (tm << 32);
-        const bool trig = ((tp >> lane) & 1u) != 0u;
-        grow = trig && (has_ref ? mx > 8.f : seen);
-        dm = grow ? mx : 0.f;
-      } else {
-        // any row with one moves up when the tile max lies above it
-        grow = has_ref ? mx > 8.f : seen;
-        dm = has_ref ? fmaxf(mx, 0.f) : (seen ? mx : 0.f);
-      }
+      const bool grow = has_ref ? mx > 8.f : seen;
       if (__any(grow)) {
+        const float dm = has_ref ? fmaxf(mx, 0.f) : (seen ? mx : 0.f);
         const float alpha = has_ref ? fast_exp2(-dm) : 0.f;  // l and O are still zero without one
         ref += dm;
         has_ref = has_ref || seen;
@@ -667,7 +630,7 @@ void attn_kernel(Args a) {
   // staged in LDS so the epilogue does not wait on memory.  Each thread's
   // first vector loads with the queries; gamma < 16 (d = 128) leaves more.
   const bool stage_dense = MODE == kSparse && a.fuse && a.gamma > 1;
-  const int per_slab = (int)fdiv((uint32_t)rows_per_block, a.fd_gamma);
+  const int per_slab = (int)fdiv((uint32_t)(kRowsPerWave * a.ppw), a.fd_gamma);
   const int nvec = stage_dense ? a.hpw * per_slab * (D / 4) : 0;
   auto dense_src = [&](int u) -> const f32x4* {
     const int slot = u / (D / 4), dv = u % (D / 4);

@@ -156,10 +156,8 @@ def test_fused_schedule_support_and_step_flags(lib):
     sup = lib.da_fused_supported
     assert sup(32, 8, 64) == 1 and sup(64, 8, 32) == 1 and sup(1, 1, 16) == 1
     assert sup(4, 1, 128) == 1 and sup(4, 1, 256) == 1 and sup(300, 300, 1) == 1
-    assert sup(4, 1, 512) == 0 and sup(6, 3, 100) == 0 and sup(1, 1, 200) == 0
-    # slabs of whole groups below the full rows, at most 1/8 of them idle: gamma 48
-    # with G 2 (240 of 256 rows), 7 with G 8 (63 of 64), 3 with G 4, 33 with G 1
-    assert sup(6, 3, 48) == 1 and sup(8, 1, 7) == 1 and sup(4, 1, 3) == 1 and sup(8, 8, 33) == 1
+    assert sup(4, 1, 512) == 0 and sup(6, 3, 48) == 0 and sup(8, 1, 7) == 0
+    assert sup(8, 2, 48) == 0 and sup(4, 1, 3) == 0 and sup(1, 1, 200) == 0
     assert sup(64, 8, 64) == 1  # G 8 takes four heads per block: 64-row slabs
     assert sup(6, 4, 64) == 0 and sup(0, 1, 64) == 0 and sup(8, 2, 0) == 0
     f = lib.delta_attn_prefill_steps
@@ -168,7 +166,7 @@ def test_fused_schedule_support_and_step_flags(lib):
         return f(FAKE, FAKE, FAKE, FAKE, None, 1, 1024, Hq, Hkv, 128, 64, 4, gamma, FAKE, 16,
                  None, steps)
     assert call(8) == 3 and call(16) == 3 and call(0) == 3 and call(7 | 16) == 3
-    assert call(7 | 8, Hq=6, Hkv=3, gamma=100) == 4  # fused schedule unavailable: rejected
+    assert call(7 | 8, Hq=6, Hkv=3, gamma=48) == 4   # fused schedule unavailable: rejected
     assert call(1 | 8) == 6 and call(7) == 6          # valid flags: the tiny workspace fails
 
 
