@@ -62,8 +62,13 @@ class DeltaAttnError(RuntimeError):
 _lib = None
 
 
-def load_library(path: str = LIB_PATH):
-    """Load the HIP library (raises if it has not been built)."""
+# DA_ABI_VERSION of include/delta_attn.h that this binding's structures follow.
+ABI_VERSION = 2
+
+
+def load_library(path: str = LIB_PATH, check_abi: bool = True):
+    """Load the HIP library (raises if it has not been built, or, with check_abi,
+    if it was built against another ABI version than this binding's)."""
     global _lib
     if _lib is not None:
         return _lib
@@ -93,6 +98,9 @@ def load_library(path: str = LIB_PATH):
     lib.da_abi_version.restype = ctypes.c_int
     lib.da_launch_plan.argtypes = [ctypes.c_int] * 7 + [ctypes.POINTER(Plan)]
     lib.da_launch_plan.restype = ctypes.c_int
+    if check_abi and lib.da_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"{path} has ABI version {lib.da_abi_version()}, this binding needs "
+                           f"{ABI_VERSION}: rebuild it with __graft_entry__.build()")
     _lib = lib
     return lib
 

@@ -256,3 +256,21 @@ def test_noalloc_call_validates_and_bounds_its_scratch_before_the_gpu(lib):
     # chunks do: that call passes this check (it then needs the GPU)
     from paper_2505_11254_amd import binding
     assert binding.workspace_bytes(1, 1 << 17, 32, 8, 128, 64) > 256 << 20
+
+
+def test_binding_abi_version_matches_header_and_library(monkeypatch):
+    """The binding's structures follow one ABI version: the header's, and the
+    built library's; a library of another version is refused at load."""
+    from paper_2505_11254_amd import binding
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    header = open(os.path.join(root, "include", "delta_attn.h")).read()
+    assert int(re.search(r"#define DA_ABI_VERSION (\d+)", header).group(1)) == binding.ABI_VERSION
+    if not os.path.exists(binding.LIB_PATH):
+        pytest.skip("library not built")
+    monkeypatch.setattr(binding, "_lib", None)
+    assert binding.load_library().da_abi_version() == binding.ABI_VERSION
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "ABI_VERSION", binding.ABI_VERSION + 1)
+    with pytest.raises(RuntimeError, match="ABI version"):
+        binding.load_library()
+    monkeypatch.setattr(binding, "_lib", None)
