@@ -8,9 +8,11 @@ and gamma from 1 to past the longest sequence.  The sparse, dense and Delta
 calls run through the C ABI, the Delta call in every schedule that applies
 (default, unfused, and fused when supported), and every output element is
 compared with the oracle.  Tolerances as elsewhere: max-abs 2e-2, mean-abs
-2e-3; the unfused schedule's second rounding (the sparse row is stored in
-bf16 before Delta is added) is forgiven in the max-abs check, up to half a
-bf16 ulp of the sparse value.  A second test draws key-block-list
+2e-3, the max-abs bound taken on top of the output's own bf16 rounding (half a
+bf16 ulp of the exact result: with a one-key window outputs reach 8 and more,
+where that rounding alone passes 2e-2) and, for the unfused schedule, of its
+second rounding (the sparse row is stored in bf16 before Delta is added), up
+to half a bf16 ulp of the sparse value.  A second test draws key-block-list
 configurations the same way (top-k, vertical-slash and Star layouts).
 """
 from __future__ import annotations
@@ -43,6 +45,18 @@ def draw(seed):
     gamma = int(rng.choice([1, 2, int(rng.integers(3, 130)), int(rng.integers(3, 130)), 64,
                             Lmax + 1]))
     return seqlens, Hkv * G, Hkv, d, window, n_sink, gamma
+
+
+def rounding_slack(ref, ref_sp, unfused):
+    """Roundings the Delta outputs are documented to make beyond the computation,
+    forgiven in the max-abs check.  Every schedule stores its output in bf16: the
+    exact result is not representable, and its nearest bf16 value lies up to half
+    a bf16 ulp away (0.031 for outputs in [8, 16), which a one-key window makes
+    possible: there the output is v_i + Delta, a sum of unit normals rather than
+    an average).  The unfused schedule also stores the sparse row in bf16 before
+    adding Delta: a second rounding, up to half a bf16 ulp of the sparse value."""
+    slack = bf16_half_ulp(ref)
+    return slack + bf16_half_ulp(ref_sp) if unfused else slack
 
 
 SEEDS = list(range(100, 132))
@@ -82,12 +96,9 @@ def test_random_configuration_matches_oracle(seed):
     assert_parity(sp, ref_sp, f"seed {seed} sparse")
     assert_parity(de, oracle.attention(*bits, cun, mode=oracle.MODE_DENSE), f"seed {seed} dense")
     for name, out in runs.items():
-        # the unfused schedule stores the sparse row in bf16 before adding Delta: a
-        # second rounding, up to half a bf16 ulp of the sparse value, which matters
-        # where outputs are O(1) (one-key windows) rather than wide averages
-        slack = bf16_half_ulp(ref_sp) if name == "unfused" or (
-            name == "default" and not lib.fused_supported(Hq, Hkv, gamma)) else None
-        assert_parity(out, ref, f"seed {seed} delta ({name})", slack=slack)
+        assert_parity(out, ref, f"seed {seed} delta ({name})",
+                      slack=rounding_slack(ref, ref_sp, unfused=name == "unfused" or (
+                          name == "default" and not lib.fused_supported(Hq, Hkv, gamma))))
 
 
 def draw_lists(seed):
@@ -154,6 +165,6 @@ def test_random_block_lists_match_oracle(seed):
                                                   block_q=block_q, gamma=gamma, return_parts=True)
     assert_parity(sp, ref_sp, f"seed {seed} sparse (lists)")
     for name, out in runs.items():
-        slack = bf16_half_ulp(ref_sp) if name == "unfused" or (
-            name == "default" and not fused_ok) else None
-        assert_parity(out, ref, f"seed {seed} delta over lists ({name})", slack=slack)
+        assert_parity(out, ref, f"seed {seed} delta over lists ({name})",
+                      slack=rounding_slack(ref, ref_sp, unfused=name == "unfused" or (
+                          name == "default" and not fused_ok)))
