@@ -149,7 +149,14 @@ int da_fused_supported(int Hq, int Hkv, int gamma);
  *                      p0 D_r, E_{-1} = D_0; c_r = E_r
  *   DA_CORR_ABG        alpha-beta-gamma filter over Delta_0, Delta_1, ...
  *                      with coefficients (p0, p1, p2) for position, velocity
- *                      and acceleration; c_r = filtered Delta_{floor(r/gamma)}
+ *                      and acceleration; c_r = filtered Delta_{floor(r/gamma)}.
+ *                      The recursion is unstable where the spectral radius of
+ *                      (I - g e0^T) F exceeds 1 (gain g = (p0, p1, p2), F the
+ *                      constant-acceleration transition with unit step), as
+ *                      for (0.05, 1.25e-4, 2.08e-5): 1.0023 per anchor.  Its
+ *                      output then grows geometrically with the anchor count,
+ *                      and so do its rounding differences from an exact
+ *                      evaluation.
  * Rows past the last whole group take the dense result.  DA_CORR_DELTA and
  * DA_CORR_RECOMPUTE take the fused schedule when da_fused_supported() (as
  * delta_attn_prefill does), the other modes the unfused one.  cu_seqlens may be
