@@ -391,6 +391,44 @@ def test_abg_matrix_reproduces_constant_and_ramp_tracking():
     assert abs((H @ ramp)[-1] - ramp[-1]) < 1e-6
 
 
+def _closed_loop_radius(a, b, c):
+    """Spectral radius of the filter's closed loop (I - g e0^T) F, from its
+    eigenvalues (unit step, constant-acceleration transition)."""
+    F = np.array([[1.0, 1.0, 0.5], [0.0, 1.0, 1.0], [0.0, 0.0, 1.0]])
+    K = np.array([[a], [b], [c]])
+    return float(max(abs(np.linalg.eigvals((np.eye(3) - K @ np.array([[1.0, 0.0, 0.0]])) @ F))))
+
+
+def test_abg_growth_over_many_anchors_matches_the_closed_loop_eigenvalue():
+    """The interpolation table's first filter setting is unstable as printed: over
+    thousands of anchors the oracle's filtered correction grows by the spectral
+    radius of the closed loop per anchor (1.0023), which a factor of 2 or 1/2 on the
+    acceleration gain would move to 1.0047 or 1.0007; the table's third setting
+    stays bounded.  gamma = 1 makes every row an anchor."""
+    (q, k, v), _, cu = rand_problem((3000,), 1, 1, 8, seed=1)
+    base = oracle.delta_attention_variant(q, k, v, cu, window=1, n_sink=0, gamma=1, mode=0,
+                                          params=(0.0, 0.0, 0.0))
+
+    def envelope(params):
+        out = oracle.delta_attention_variant(q, k, v, cu, window=1, n_sink=0, gamma=1, mode=4,
+                                             params=params)
+        c = np.abs(out - base)[:, 0, :]
+        return c[2000:2500].max(), c[2500:3000].max()
+
+    p = (0.05, 1.25e-4, 2.08e-5)
+    rho = _closed_loop_radius(*p)
+    assert rho > 1.002
+    m1, m2 = envelope(p)
+    rate = (m2 / m1) ** (1.0 / 500)
+    assert abs(rate - rho) < 3e-4, (rate, rho)
+    for alt in (2.0, 0.5):
+        assert abs(rate - _closed_loop_radius(p[0], p[1], p[2] * alt)) > 1e-3
+    p = (0.2, 5e-2, 3.5e-3)
+    assert _closed_loop_radius(*p) < 1.0
+    m1, m2 = envelope(p)
+    assert m2 < 10.0 and m2 < 2 * m1
+
+
 VARIANT_MUTANTS = {
     "interp_beta_over_gamma": ("(double)kk / (double)(gamma - 1)", "(double)kk / (double)gamma"),
     # (starting the EMA from 0 instead of D_0 is no mistake: anchor 0 only sees key 0,
