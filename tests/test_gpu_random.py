@@ -13,7 +13,9 @@ bf16 ulp of the exact result: with a one-key window outputs reach 8 and more,
 where that rounding alone passes 2e-2) and, for the unfused schedule, of its
 second rounding (the sparse row is stored in bf16 before Delta is added), up
 to half a bf16 ulp of the sparse value.  A second test draws key-block-list
-configurations the same way (top-k, vertical-slash and Star layouts).
+configurations the same way (top-k, vertical-slash and Star layouts), and a
+third longer ones, of 2.5K-24K tokens, whose dense rows span several key
+chunks.
 """
 from __future__ import annotations
 
@@ -59,14 +61,44 @@ def rounding_slack(ref, ref_sp, unfused):
     return slack + bf16_half_ulp(ref_sp) if unfused else slack
 
 
+def draw_long(seed):
+    """A configuration long enough for several key chunks per dense row (a chunk
+    holds at least 2560 keys): 2.5K-24K tokens, GQA 1-4, gamma 8-129."""
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 4))
+    if rng.random() < 0.4:
+        seqlens = (int(rng.integers(2500, 16000)),) * B
+    else:
+        seqlens = tuple(int(x) for x in rng.integers(1, 24000, B))
+    Hkv = int(rng.choice([1, 2]))
+    G = int(rng.choice([1, 2, 4]))
+    d = int(rng.choice([64, 64, 128]))
+    Lmax = max(seqlens)
+    window = int(rng.choice([1, int(rng.integers(1, 1100)), int(rng.integers(1, 1100)),
+                             Lmax + int(rng.integers(0, 50))]))
+    n_sink = int(rng.choice([0, int(rng.integers(0, 8)), int(rng.integers(0, 300))]))
+    gamma = int(rng.choice([8, 16, int(rng.integers(8, 130)), 64]))
+    return seqlens, Hkv * G, Hkv, d, window, n_sink, gamma
+
+
 SEEDS = list(range(100, 132))
+LONG_SEEDS = [30000, 30003, 30007, 30008, 30010, 30011, 30012, 30015]
 
 
 @pytest.mark.parametrize("seed", SEEDS)
 def test_random_configuration_matches_oracle(seed):
+    check_configuration(seed, draw(seed))
+
+
+@pytest.mark.parametrize("seed", LONG_SEEDS)
+def test_random_long_configuration_matches_oracle(seed):
+    check_configuration(seed, draw_long(seed))
+
+
+def check_configuration(seed, cfg):
     from paper_2505_11254_amd import binding as lib
     from paper_2505_11254_amd.inputs import random_qkv
-    seqlens, Hq, Hkv, d, w, s, gamma = draw(seed)
+    seqlens, Hq, Hkv, d, w, s, gamma = cfg
     print(f"seed {seed}: seqlens={seqlens} Hq={Hq} Hkv={Hkv} d={d} window={w} n_sink={s} "
           f"gamma={gamma}", flush=True)
     q, k, v, cu = random_qkv(seqlens, Hq, Hkv, d, seed=seed)
