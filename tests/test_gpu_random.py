@@ -15,7 +15,8 @@ second rounding (the sparse row is stored in bf16 before Delta is added), up
 to half a bf16 ulp of the sparse value.  A second test draws key-block-list
 configurations the same way (top-k, vertical-slash and Star layouts), and a
 third longer ones, of 2.5K-24K tokens, whose dense rows span several key
-chunks.
+chunks, and a fourth edge-shaped ones (empty sequences, GQA ratios 5-7,
+sinks and gamma past the sequence).
 """
 from __future__ import annotations
 
@@ -81,8 +82,34 @@ def draw_long(seed):
     return seqlens, Hkv * G, Hkv, d, window, n_sink, gamma
 
 
+def draw_edge(seed):
+    """An edge-shaped configuration: ragged batches of up to 4 with empty
+    sequences, every GQA ratio 1-8 over up to 3 kv heads, sinks up to 2000
+    (past the sequence), gamma up to three times the longest sequence."""
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 5))
+    seqlens = [int(x) for x in rng.integers(1, 1500, B)]
+    for i in range(B):
+        if rng.random() < 0.3:
+            seqlens[i] = 0
+    if max(seqlens) == 0:
+        seqlens[int(rng.integers(0, B))] = int(rng.integers(1, 1500))
+    seqlens = tuple(seqlens)
+    Hkv = int(rng.choice([1, 2, 3]))
+    G = int(rng.integers(1, 9))
+    d = int(rng.choice([64, 128]))
+    Lmax = max(seqlens)
+    window = int(rng.choice([1, int(rng.integers(1, 600)), Lmax + int(rng.integers(0, 50))]))
+    n_sink = int(rng.choice([0, int(rng.integers(0, 8)), int(rng.integers(0, 2000))]))
+    gamma = int(rng.choice([1, 2, int(rng.integers(3, 130)), Lmax + 1, 3 * Lmax + 7]))
+    return seqlens, Hkv * G, Hkv, d, window, n_sink, gamma
+
+
 SEEDS = list(range(100, 132))
 LONG_SEEDS = [30000, 30003, 30007, 30008, 30010, 30011, 30012, 30015]
+# empty sequences with: sinks and gamma past the sequence; G 5 on 3 kv heads; G 7
+# with sinks past it; G 6 on 3 kv heads with gamma 2; G 7, gamma past it; G 5
+EDGE_SEEDS = [80004, 80012, 80013, 80028, 80041, 80054]
 
 
 @pytest.mark.parametrize("seed", SEEDS)
@@ -93,6 +120,11 @@ def test_random_configuration_matches_oracle(seed):
 @pytest.mark.parametrize("seed", LONG_SEEDS)
 def test_random_long_configuration_matches_oracle(seed):
     check_configuration(seed, draw_long(seed))
+
+
+@pytest.mark.parametrize("seed", EDGE_SEEDS)
+def test_random_edge_configuration_matches_oracle(seed):
+    check_configuration(seed, draw_edge(seed))
 
 
 def check_configuration(seed, cfg):
